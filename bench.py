@@ -1,0 +1,290 @@
+#!/usr/bin/env python3
+"""Benchmark: BITCOS ternary GEMV effective weight bandwidth on one MI355X.
+
+A step is one batch-1 pass over a whole decode layer set (every GEMV of every
+layer, inputs already resident in HBM), replayed from a HIP graph.  The
+headline is the BitNet-2B-like set: 30 layers x {q, o 2560x2560; k, v
+640x2560; gate, up 6912x2560; down 2560x6912}, z = 0.42 iid, one fp16 scale
+per tensor, bf16 activations ~ N(0, 1) (the int8-quantised variant is reported
+beside it).  value = sum of BITCOS payload bytes (bitmap + signs + scales) /
+step time.  The same step over the five-trit and 2-bit layouts of the same
+weights gives the same-GPU speedups.
+
+Prints ONE JSON line.  See the design doc for the roofline and CPU-baseline
+definitions.
+"""
+
+from __future__ import annotations
+
+import argparse
+import concurrent.futures as cf
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import workloads as wl  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "ternary GEMV effective weight GB/s (% of 8 TB/s HBM peak); speedup vs 5-trit"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="bitnet2b_layers")
+    ap.add_argument("--layers", type=int, default=0, help="0 = the workload's layer count")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-baselines", action="store_true", help="skip the five-trit / 2-bit steps")
+    ap.add_argument("--threads", type=int, default=min(16, os.cpu_count() or 1))
+    return ap.parse_args()
+
+
+def build_set(wk, layers, fmts, threads):
+    """Pack every matrix of the layer set in every format (host), upload to HBM."""
+    import torch
+
+    from paper_2609_16338_amd import api
+
+    jobs = [(l, mi, spec) for l in range(layers) for mi, spec in enumerate(wk.matrices)]
+
+    def one(job):
+        l, mi, spec = job
+        w, sc = wl.matrix_inputs(wk.cid, l, mi, spec)
+        out = {}
+        for fmt in fmts:
+            L, blob = api.plan_and_pack(fmt, w, sc, spec.group)
+            out[fmt] = (L, blob)
+        return job, out
+
+    packed = {}
+    with cf.ThreadPoolExecutor(max_workers=threads) as ex:
+        for (l, mi, spec), out in ex.map(one, jobs):
+            for fmt, (L, blob) in out.items():
+                packed.setdefault(fmt, []).append((l, mi, spec, L, torch.from_numpy(blob).cuda()))
+    return packed
+
+
+def activations(wk, kinds):
+    """Per distinct K: device activations (bf16, and int8 + per-group scales via the library)."""
+    import torch
+
+    from paper_2609_16338_amd import api
+
+    acts = {}
+    for k in sorted({s.k for s in wk.matrices}):
+        xb = wl.activation_inputs(wk.cid, "bf16", 1, k)
+        xbd = torch.from_numpy(xb.view(np.int16)).view(torch.bfloat16).cuda()
+        acts[("bf16", k)] = (xbd, None)
+        if "int8" in kinds:
+            q = torch.empty((1, k), dtype=torch.int8, device="cuda")
+            a = torch.empty((1, k // 128), dtype=torch.float32, device="cuda")
+            api.quantize_activations(xbd, q, a)
+            acts[("int8", k)] = (q, a)
+    torch.cuda.synchronize()
+    return acts
+
+
+def make_step(entries, acts, kind):
+    import torch
+
+    from paper_2609_16338_amd import api
+
+    ys = [torch.empty((1, L.n), dtype=torch.float32, device="cuda") for (_, _, _, L, _) in entries]
+
+    def step():
+        for (l, mi, spec, L, blob), y in zip(entries, ys):
+            x, xs = acts[(kind, spec.k)]
+            api.gemv(L, blob, x, y, xs)
+    return step, ys
+
+
+def capture(step):
+    import torch
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    torch.cuda.synchronize()
+    return g
+
+
+def time_graph(g, steps, warmup):
+    import torch
+    for _ in range(warmup):
+        g.replay()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    start.record()
+    for _ in range(steps):
+        g.replay()
+    end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    return start.elapsed_time(end) / steps, wall
+
+
+def cpu_baseline(wk, budget_s=12.0):
+    """The oracle (decode + dense GEMV) on the host, on whole matrices of layer 0."""
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        cores = os.cpu_count() or 1
+    done_w = 0
+    done_bytes = 0
+    t_total = 0.0
+    mats = 0
+    t_start = time.perf_counter()
+    while time.perf_counter() - t_start < budget_s:
+        for mi, spec in enumerate(wk.matrices):
+            w, sc = wl.matrix_inputs(wk.cid, 0, mi, spec)
+            xb = wl.activation_inputs(wk.cid, "bf16", 1, spec.k)
+            p = O.bitcos_encode(w, sc, spec.group, 1)
+            t0 = time.perf_counter()
+            wd, sd = O.bitcos_decode(p)
+            O.dense_gemv(wd, sd, spec.group, xb, x_is_bf16_bits=True)
+            t_total += time.perf_counter() - t0
+            done_w += spec.n * spec.k
+            done_bytes += O.payload_bits(p) / 8
+            mats += 1
+            if time.perf_counter() - t_start >= budget_s:
+                break
+    return {
+        "value": round(done_bytes / t_total / 1e9, 4),
+        "unit": "GB/s",
+        "cores": int(cores),
+        "kind": "oracle",
+        "sample": f"{mats} matrices of layer 0 of {wk.name} (decode + dense bf16 GEMV, "
+                  f"{done_w / 1e6:.1f} M weights, {t_total:.1f} s)",
+        "weights_per_s": round(done_w / t_total, 1),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        sys.exit(2)
+    import torch
+
+    from paper_2609_16338_amd import _native as N
+    from paper_2609_16338_amd import api
+
+    N.lib()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    wk = wl.WORKLOADS[args.workload]
+    layers = args.layers or wk.layers
+    fmts = [N.FMT_BITCOS] + ([] if args.no_baselines else [N.FMT_TRIT5, N.FMT_BIT2])
+    t0 = time.perf_counter()
+    packed = build_set(wk, layers, fmts, args.threads)
+    acts = activations(wk, ("bf16", "int8"))
+    prep_s = time.perf_counter() - t0
+    print(f"[bench] packed {layers} layers x {len(wk.matrices)} matrices in {prep_s:.1f} s", file=sys.stderr, flush=True)
+
+    payload = {fmt: sum(e[3].payload_bits for e in ents) / 8 for fmt, ents in packed.items()}
+    weights = sum(e[3].n * e[3].k for e in packed[N.FMT_BITCOS])
+    res = {}
+    for fmt in fmts:
+        for kind in ("bf16", "int8"):
+            step, _ = make_step(packed[fmt], acts, kind)
+            g = capture(step)
+            ms, wall = time_graph(g, args.steps, args.warmup)
+            res[(fmt, kind)] = ms
+            print(f"[bench] fmt={fmt} {kind}: {ms * 1e3:.1f} us/step, "
+                  f"{payload[fmt] / (ms * 1e-3) / 1e9:.1f} GB/s", file=sys.stderr, flush=True)
+            del g
+
+    # Dominant kernel: the BITCOS GEMV instantiation that handles most of the
+    # bytes (K = 2560 for this set), timed on its own graph of the gate
+    # matrices of every layer (distinct buffers, so nothing is cache-resident).
+    gate = [e for e in packed[N.FMT_BITCOS] if e[2].name == "gate"]
+    step_g, _ = make_step(gate, acts, "bf16")
+    gg = capture(step_g)
+    ms_g, _ = time_graph(gg, args.steps, args.warmup)
+    per_launch_us = ms_g * 1e3 / len(gate)
+    L0 = gate[0][3]
+    alg_bytes = L0.payload_bits / 8 + L0.k * 2 + L0.n * 4
+    info = api.describe(L0, 1, N.X_BF16)
+    achieved = alg_bytes / (per_launch_us * 1e-6) / 1e9
+
+    ms = res[(N.FMT_BITCOS, "bf16")]
+    value = payload[N.FMT_BITCOS] / (ms * 1e-3) / 1e9
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{wk.name}: {layers} layers x {{q,o {wk.matrices[0].n}x{wk.matrices[0].k}; "
+                        f"k,v {wk.matrices[1].n}x{wk.matrices[1].k}; gate,up {wk.matrices[4].n}x{wk.matrices[4].k}; "
+                        f"down {wk.matrices[6].n}x{wk.matrices[6].k}}}, z={wk.matrices[0].z} iid, "
+                        f"{'per-tensor' if wk.matrices[0].group == 0 else 'group-128'} fp16 scales, "
+                        "bf16 x ~ N(0,1), batch 1",
+            "global_batch": 1,
+            "layers": layers,
+            "gemvs_per_step": len(packed[N.FMT_BITCOS]),
+            "weights_per_step": weights,
+            "payload_bytes_per_step": int(payload[N.FMT_BITCOS]),
+        },
+        "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
+        "weights_per_s": float(f"{weights / (ms * 1e-3):.4g}"),
+        "bpw_payload": round(payload[N.FMT_BITCOS] * 8 / weights, 5),
+    }
+    if N.FMT_TRIT5 in fmts:
+        out["speedup_vs_trit5"] = round(res[(N.FMT_TRIT5, "bf16")] / ms, 4)
+        out["speedup_vs_bit2"] = round(res[(N.FMT_BIT2, "bf16")] / ms, 4)
+        out["baselines_us_per_step"] = {
+            "trit5_bf16": round(res[(N.FMT_TRIT5, "bf16")] * 1e3, 2),
+            "bit2_bf16": round(res[(N.FMT_BIT2, "bf16")] * 1e3, 2),
+            "trit5_int8": round(res[(N.FMT_TRIT5, "int8")] * 1e3, 2),
+            "bit2_int8": round(res[(N.FMT_BIT2, "int8")] * 1e3, 2),
+        }
+    ms8 = res[(N.FMT_BITCOS, "int8")]
+    out["int8_variant"] = {
+        "value": round(payload[N.FMT_BITCOS] / (ms8 * 1e-3) / 1e9, 2),
+        "ms_per_step": round(ms8, 5),
+        "speedup_vs_trit5": round(res[(N.FMT_TRIT5, "int8")] / ms8, 4) if N.FMT_TRIT5 in fmts else None,
+        "speedup_vs_bit2": round(res[(N.FMT_BIT2, "int8")] / ms8, 4) if N.FMT_TRIT5 in fmts else None,
+    }
+    out["roofline"] = {
+        "bound": "hbm",
+        "achieved": round(achieved, 2),
+        "peak": HBM_PEAK_GBS,
+        "unit": "GB/s",
+        "frac": round(achieved / HBM_PEAK_GBS, 4),
+        "traffic": None,
+        "kernel": f"bitcos_gemv_kernel<{info.per_lane},{info.seg_lanes},bf16> on gate {L0.n}x{L0.k}",
+        "per_launch_us": round(per_launch_us, 3),
+        "bytes_per_launch": int(alg_bytes),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wk)
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

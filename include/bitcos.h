@@ -1,0 +1,211 @@
+/*
+ * bitcos.h -- C ABI of libbitcos: ternary GEMV over the BITCOS layout on MI355X (gfx950).
+ *
+ * BITCOS (paper "Breaking the 1.58-bit Barrier for Ternary LLMs", Sec. II-A)
+ * stores a ternary matrix W in {-1, 0, +1}^{N x K} as
+ *   - a presence bitmap with one bit per weight, set where the weight is
+ *     non-zero, and
+ *   - a sign vector with one bit per NON-ZERO weight, in the same tensor order
+ *     (the j-th sign bit belongs to the j-th set bit of the bitmap; a set sign
+ *     bit means -1, Sec. II-D Eq. (4)),
+ * which costs 2 - z bits per weight at zero density z (Eq. (1)).  Beside the
+ * two streams the blob carries non-negative fp16 scales (one per 128 weights
+ * along K, or one per tensor) and 32-bit sign offsets, one per "unit" of
+ * rows, telling where each unit enters the sign stream (the paper leaves the
+ * storage of stream entry points open, Sec. II-D; these offsets are metadata
+ * outside the 2 - z payload).
+ *
+ * The GEMV computes y = (S (.) W) x for one activation row (batch 1 decode):
+ *   y[n] = sum_g S[n, g] * a[g] * sum_{k in group g} W[n, k] * x[k]
+ * with int8 activations accumulated exactly in int32 and the group scale
+ * applied once per group (Sec. II-C), or bf16 activations accumulated in
+ * fp32.  Two same-GPU baselines use fixed-rate layouts: five trits per byte,
+ * 26 bytes per 128 weights (Sec. I), and 2 bits per weight (Table I).
+ *
+ * Layouts (all little-endian; every section starts at a 256-byte boundary
+ * of the blob and the blob length is a multiple of 256 bytes):
+ *   BITCOS  section 0  bitmap   u32[N*K/32]; bit b of word w is weight
+ *                               32w + b of W in row-major (n, k) order.
+ *           section 1  signs    u32[ceil(nnz/32)] LSB-first sign stream,
+ *                               then 16 zero bytes (the GEMV may read them).
+ *           section 2  offsets  u32[ceil(N/unit_rows) + 1]; entry u is the
+ *                               number of non-zeros in rows
+ *                               [0, u*unit_rows); the last entry is nnz.
+ *           section 3  scales   fp16[N][K/128] (group 128) or fp16[1].
+ *   TRIT5   section 0  codes    26-byte blocks, row-major [N][K/128]; byte j
+ *                               of a block holds weights 5j..5j+4 of the
+ *                               block as sum_t (w+1) * 3^t (a missing weight
+ *                               past 127 is the digit 1), then 16 zero bytes.
+ *           section 3  scales   as BITCOS.
+ *   BIT2    section 0  codes    u32 per 16 weights, row-major; weight
+ *                               k0 + 4t + b (k0 = 16 * word) has the code
+ *                               w + 1 at bits [8b + 2t, 8b + 2t + 1].
+ *           section 3  scales   as BITCOS.
+ *
+ * Conventions for every function:
+ *   - Return BITCOS_OK (0) or a negative status; nothing aborts or prints.
+ *     bitcos_strerror() names a status.  All validation happens before any
+ *     device work is enqueued.
+ *   - The caller owns every host and device buffer and the stream; the
+ *     library allocates nothing on the device, keeps no mutable global state
+ *     and is safe to call from several threads.
+ *   - Device pointers are plain device addresses (e.g. a torch tensor's
+ *     data_ptr()); `stream` is a hipStream_t passed as void* (NULL = the
+ *     default stream).  GEMV calls are asynchronous and never synchronise.
+ *   - Host pointers are ordinary host memory.
+ */
+#ifndef BITCOS_H
+#define BITCOS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------ */
+#define BITCOS_OK 0
+#define BITCOS_E_ARG (-1)          /* null pointer, bad size/shape/enum      */
+#define BITCOS_E_VALUE (-2)        /* weight outside {-1,0,1}, bad scale, corrupt blob */
+#define BITCOS_E_SPACE (-3)        /* destination capacity too small          */
+#define BITCOS_E_HIP (-4)          /* HIP launch/runtime error                */
+#define BITCOS_E_UNSUPPORTED (-5)  /* shape/dtype/batch without a kernel      */
+
+/* ---- enums ------------------------------------------------------------- */
+#define BITCOS_LAYOUT_VERSION 1u
+
+#define BITCOS_FMT_BITCOS 1
+#define BITCOS_FMT_TRIT5 2
+#define BITCOS_FMT_BIT2 3
+
+#define BITCOS_SEC_BITMAP 0   /* BITCOS */
+#define BITCOS_SEC_SIGNS 1    /* BITCOS */
+#define BITCOS_SEC_OFFSETS 2  /* BITCOS */
+#define BITCOS_SEC_CODES 0    /* TRIT5, BIT2 */
+#define BITCOS_SEC_SCALES 3   /* all formats */
+
+#define BITCOS_X_I8 1         /* activations int8 [m][K]                 */
+#define BITCOS_X_BF16 2       /* activations bfloat16 bit patterns [m][K] */
+
+#define BITCOS_Y_F32 1        /* y float32 [m][N], scaled                 */
+#define BITCOS_Y_I32_RAW 2    /* y int32 [m][N] = sum_k W x, unscaled (int8 x only) */
+
+/* Plain-old-data description of one packed matrix.  Filled by *_plan();
+ * passed by pointer to pack/unpack/gemv.  Section offsets are relative to the
+ * blob start. */
+typedef struct bitcos_layout {
+  uint32_t version;        /* BITCOS_LAYOUT_VERSION                           */
+  uint32_t format;         /* BITCOS_FMT_*                                    */
+  int32_t n;               /* output rows N (>= 1)                            */
+  int32_t k;               /* reduction length K                              */
+  int32_t group;           /* 128: one scale per 128 weights of a row; 0: one per tensor */
+  int32_t unit_rows;       /* BITCOS: rows per sign-offset entry; 0 otherwise */
+  uint64_t nnz;            /* number of non-zero weights                     */
+  uint64_t sec_off[4];     /* byte offset of each section (0 if unused)      */
+  uint64_t sec_bytes[4];   /* byte length of each section (0 if unused)      */
+  uint64_t total_bytes;    /* blob length (multiple of 256)                  */
+  uint64_t payload_bits;   /* format symbols + 16-bit scales, no metadata    */
+} bitcos_layout;
+
+/* Name of a status code (static string; never NULL). */
+const char* bitcos_strerror(int status);
+
+/* BITCOS_LAYOUT_VERSION of the library. */
+uint32_t bitcos_version(void);
+
+/* ---- BITCOS -------------------------------------------------------------
+ * bitcos_plan: validate W (host int8 [n][k], row-major, values in {-1,0,1})
+ * and fill *out.  group is 128 (k % 128 == 0) or 0 (one scale per tensor,
+ * k % 32 == 0).  unit_rows >= 1 sets the rows per sign offset; 0 picks the
+ * library default for (n, k) (the GEMV's rows per wave).  Errors: E_ARG,
+ * E_VALUE (a weight outside {-1,0,1}).  Paper: Sec. II-A. */
+int bitcos_plan(const int8_t* w, int32_t n, int32_t k, int32_t group, int32_t unit_rows,
+                bitcos_layout* out);
+
+/* bitcos_pack: write the whole blob for W and its scales (host fp16 bit
+ * patterns, [n][k/128] or [1]; finite and non-negative) into host memory
+ * dst of `cap` bytes (>= L->total_bytes).  Bytes are a deterministic
+ * function of (W, scales, *L); padding is zero.  Errors: E_ARG, E_VALUE
+ * (bad weight or scale, W not the one planned), E_SPACE. */
+int bitcos_pack(const int8_t* w, const uint16_t* scales_f16, const bitcos_layout* L, void* dst,
+                size_t cap);
+
+/* bitcos_unpack: exact inverse of bitcos_pack on a host blob of
+ * `blob_bytes` bytes: writes W (host int8 [n][k]) and the scales (host
+ * fp16 bits).  Verifies the bitmap popcount against nnz and every unit
+ * offset; E_VALUE on a mismatch. */
+int bitcos_unpack(const bitcos_layout* L, const void* blob, size_t blob_bytes, int8_t* w_out,
+                  uint16_t* scales_out);
+
+/* bitcos_gemv: y = (S (.) W) x on the device, enqueued on `stream`.
+ *   blob_dev  device copy of the packed blob (L->total_bytes bytes).
+ *   m         number of activation rows; 1 (batch-1 decode).
+ *   x_dev     device activations [m][k]: int8 (BITCOS_X_I8) or bf16 bits
+ *             (BITCOS_X_BF16), row-major.
+ *   xscale_dev  NULL (a = 1) or device fp32 [m][k/128] per-group activation
+ *             scales a (int8 activations quantised per group of 128).
+ *   y_dev     device output [m][n], overwritten: fp32 (BITCOS_Y_F32) or the
+ *             unscaled int32 row sums (BITCOS_Y_I32_RAW, int8 x only, exact).
+ * int8 x accumulates exactly in int32 per group and applies the scale once per
+ * group in fp32; with one scale per tensor and no xscale the full int32 row
+ * sum is multiplied once.  bf16 x accumulates in fp32.
+ * Errors: E_ARG, E_UNSUPPORTED (m, dtype or shape without a kernel), E_HIP. */
+int bitcos_gemv(const bitcos_layout* L, const void* blob_dev, int32_t m, const void* x_dev,
+                int32_t x_dtype, const float* xscale_dev, void* y_dev, int32_t y_mode,
+                void* stream);
+
+/* ---- five-trit baseline (26 B per 128 weights; Sec. I) -------------------
+ * Same conventions as the BITCOS functions; k % 128 == 0 always (the block is
+ * 128 weights whatever the scale group). */
+int trit5_plan(const int8_t* w, int32_t n, int32_t k, int32_t group, bitcos_layout* out);
+int trit5_pack(const int8_t* w, const uint16_t* scales_f16, const bitcos_layout* L, void* dst,
+               size_t cap);
+int trit5_unpack(const bitcos_layout* L, const void* blob, size_t blob_bytes, int8_t* w_out,
+                 uint16_t* scales_out);
+int trit5_gemv(const bitcos_layout* L, const void* blob_dev, int32_t m, const void* x_dev,
+               int32_t x_dtype, const float* xscale_dev, void* y_dev, int32_t y_mode,
+               void* stream);
+
+/* ---- 2-bit baseline (2 bits per weight; Table I) ------------------------ */
+int bit2_plan(const int8_t* w, int32_t n, int32_t k, int32_t group, bitcos_layout* out);
+int bit2_pack(const int8_t* w, const uint16_t* scales_f16, const bitcos_layout* L, void* dst,
+              size_t cap);
+int bit2_unpack(const bitcos_layout* L, const void* blob, size_t blob_bytes, int8_t* w_out,
+                uint16_t* scales_out);
+int bit2_gemv(const bitcos_layout* L, const void* blob_dev, int32_t m, const void* x_dev,
+              int32_t x_dtype, const float* xscale_dev, void* y_dev, int32_t y_mode,
+              void* stream);
+
+/* ---- activation quantisation --------------------------------------------
+ * bitcos_quantize_act: int8 activations for the int8 GEMV path, quantised per
+ * group of 128 (Sec. II-C).  The paper does not state the rule; this one is
+ * symmetric absmax: for every row r and group g,
+ *   a[r][g] = max|x| / 127 in fp32 (1 for an all-zero group),
+ *   q[r][k] = clamp(round_half_even(x / a), -127, 127), divisions IEEE fp32.
+ * x_bf16_dev: device bf16 bits [m][k]; q_dev: device int8 [m][k]; scale_dev:
+ * device fp32 [m][k/128] (pass it as the GEMV's xscale_dev).  k % 128 == 0.
+ * Asynchronous on `stream`.  Errors: E_ARG, E_UNSUPPORTED, E_HIP. */
+int bitcos_quantize_act(const void* x_bf16_dev, int32_t m, int32_t k, int8_t* q_dev,
+                        float* scale_dev, void* stream);
+
+/* ---- launch description (for measurement) ---------------------------------
+ * Fills the kernel configuration a GEMV on this layout would launch with:
+ * words (or blocks) per lane, lanes per row segment, rows per wave step,
+ * waves and workgroups.  Errors as for the GEMV. */
+typedef struct bitcos_launch_info {
+  int32_t per_lane;        /* BITCOS: 32-weight words per lane; TRIT5: 128-blocks; BIT2: 16-weight words */
+  int32_t seg_lanes;       /* lanes that share one row (power of two)          */
+  int32_t rows_per_step;   /* rows a wave covers per step = 64 / seg_lanes      */
+  int32_t lanes_used;      /* lanes per row that hold weights                   */
+  int64_t waves;           /* waves launched                                   */
+  int64_t workgroups;      /* workgroups launched (256 threads each)           */
+} bitcos_launch_info;
+
+int bitcos_describe(const bitcos_layout* L, int32_t m, int32_t x_dtype, bitcos_launch_info* out);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BITCOS_H */

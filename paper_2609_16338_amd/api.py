@@ -1,0 +1,211 @@
+"""Python binding of libbitcos: the C ABI's functions under the same names.
+
+Argument marshalling only -- every step of the GEMV runs in the HIP kernels of
+libbitcos.so; packing runs in its C++ host code.  Host arrays are numpy;
+device buffers are torch tensors (torch supplies device memory and streams).
+Sizes of device buffers are checked here, before the call, because the C ABI
+takes plain pointers.
+"""
+
+from __future__ import annotations
+
+import ctypes
+
+import numpy as np
+
+from . import _native as N
+from ._native import (FMT_BIT2, FMT_BITCOS, FMT_TRIT5, LaunchInfo, Layout, X_BF16, X_I8,  # noqa: F401
+                      Y_F32, Y_I32_RAW)
+
+
+def _ptr(a: np.ndarray) -> ctypes.c_void_p:
+    return ctypes.c_void_p(a.ctypes.data)
+
+
+def _w(w) -> np.ndarray:
+    w = np.ascontiguousarray(w)
+    if w.dtype != np.int8 or w.ndim != 2:
+        raise ValueError("W must be a 2-D int8 array")
+    return w
+
+
+def _scales(s) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(s).view(np.uint16) if np.asarray(s).dtype == np.float16
+                                else np.asarray(s, dtype=np.uint16)).reshape(-1)
+
+
+def num_scales(L: Layout) -> int:
+    return L.n * (L.k // 128) if L.group == 128 else 1
+
+
+# ---------------------------------------------------------------------------
+# plan / pack / unpack (host)
+# ---------------------------------------------------------------------------
+
+def bitcos_plan(w, group: int = 128, unit_rows: int = 0) -> Layout:
+    w = _w(w)
+    L = Layout()
+    N.check(N.lib().bitcos_plan(_ptr(w), w.shape[0], w.shape[1], group, unit_rows, ctypes.byref(L)),
+            "bitcos_plan")
+    return L
+
+
+def trit5_plan(w, group: int = 128) -> Layout:
+    w = _w(w)
+    L = Layout()
+    N.check(N.lib().trit5_plan(_ptr(w), w.shape[0], w.shape[1], group, ctypes.byref(L)), "trit5_plan")
+    return L
+
+
+def bit2_plan(w, group: int = 128) -> Layout:
+    w = _w(w)
+    L = Layout()
+    N.check(N.lib().bit2_plan(_ptr(w), w.shape[0], w.shape[1], group, ctypes.byref(L)), "bit2_plan")
+    return L
+
+
+def _pack(fn: str, w, scales, L: Layout) -> np.ndarray:
+    w = _w(w)
+    s = _scales(scales)
+    if w.shape != (L.n, L.k) or s.size != num_scales(L):
+        raise ValueError("W or scales do not match the layout")
+    out = np.empty(L.total_bytes, dtype=np.uint8)
+    N.check(getattr(N.lib(), fn)(_ptr(w), _ptr(s), ctypes.byref(L), _ptr(out), out.nbytes), fn)
+    return out
+
+
+def bitcos_pack(w, scales, L: Layout) -> np.ndarray:
+    return _pack("bitcos_pack", w, scales, L)
+
+
+def trit5_pack(w, scales, L: Layout) -> np.ndarray:
+    return _pack("trit5_pack", w, scales, L)
+
+
+def bit2_pack(w, scales, L: Layout) -> np.ndarray:
+    return _pack("bit2_pack", w, scales, L)
+
+
+def _unpack(fn: str, L: Layout, blob) -> tuple[np.ndarray, np.ndarray]:
+    blob = np.ascontiguousarray(blob, dtype=np.uint8)
+    w = np.empty((L.n, L.k), dtype=np.int8)
+    s = np.empty(num_scales(L), dtype=np.uint16)
+    N.check(getattr(N.lib(), fn)(ctypes.byref(L), _ptr(blob), blob.nbytes, _ptr(w), _ptr(s)), fn)
+    return w, s
+
+
+def bitcos_unpack(L: Layout, blob):
+    return _unpack("bitcos_unpack", L, blob)
+
+
+def trit5_unpack(L: Layout, blob):
+    return _unpack("trit5_unpack", L, blob)
+
+
+def bit2_unpack(L: Layout, blob):
+    return _unpack("bit2_unpack", L, blob)
+
+
+def plan_and_pack(fmt: int, w, scales, group: int = 128, unit_rows: int = 0):
+    """(layout, host blob) for one of the three formats."""
+    if fmt == FMT_BITCOS:
+        L = bitcos_plan(w, group, unit_rows)
+        return L, bitcos_pack(w, scales, L)
+    if fmt == FMT_TRIT5:
+        L = trit5_plan(w, group)
+        return L, trit5_pack(w, scales, L)
+    if fmt == FMT_BIT2:
+        L = bit2_plan(w, group)
+        return L, bit2_pack(w, scales, L)
+    raise ValueError(f"unknown format {fmt}")
+
+
+# ---------------------------------------------------------------------------
+# GEMV (device)
+# ---------------------------------------------------------------------------
+
+_GEMV = {FMT_BITCOS: "bitcos_gemv", FMT_TRIT5: "trit5_gemv", FMT_BIT2: "bit2_gemv"}
+
+
+def _stream_handle(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def gemv(L: Layout, blob_dev, x, y, xscale=None, y_mode: int = Y_F32, stream=None):
+    """Enqueue y = (S (.) W) x for the layout's format on `stream`.
+
+    blob_dev: uint8 cuda tensor of >= L.total_bytes; x: int8 or bfloat16 cuda
+    tensor [m, k] (or [k]); y: float32 (Y_F32) or int32 (Y_I32_RAW) cuda
+    tensor [m, n] (or [n]); xscale: None or float32 cuda tensor [m, k/128].
+    """
+    import torch
+    m = x.shape[0] if x.dim() == 2 else 1
+    if x.dtype == torch.int8:
+        xd = X_I8
+    elif x.dtype == torch.bfloat16:
+        xd = X_BF16
+    else:
+        raise TypeError("x must be int8 or bfloat16")
+    for t, nm in ((blob_dev, "blob"), (x, "x"), (y, "y")):
+        if not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{nm} must be a contiguous cuda tensor")
+    if blob_dev.dtype != torch.uint8 or blob_dev.numel() < L.total_bytes:
+        raise ValueError("blob_dev must be uint8 with at least total_bytes elements")
+    if x.numel() != m * L.k:
+        raise ValueError("x has the wrong size")
+    want_y = torch.int32 if y_mode == Y_I32_RAW else torch.float32
+    if y.dtype != want_y or y.numel() != m * L.n:
+        raise ValueError("y has the wrong dtype or size")
+    xs_ptr = None
+    if xscale is not None:
+        if (not xscale.is_cuda or xscale.dtype != torch.float32 or not xscale.is_contiguous()
+                or xscale.numel() != m * (L.k // 128) or L.k % 128):
+            raise ValueError("xscale must be a contiguous float32 cuda tensor [m, k/128]")
+        xs_ptr = ctypes.c_void_p(xscale.data_ptr())
+    fn = getattr(N.lib(), _GEMV[L.format])
+    st = fn(ctypes.byref(L), ctypes.c_void_p(blob_dev.data_ptr()), m, ctypes.c_void_p(x.data_ptr()), xd,
+            xs_ptr, ctypes.c_void_p(y.data_ptr()), y_mode, _stream_handle(stream))
+    N.check(st, _GEMV[L.format])
+    return y
+
+
+def bitcos_gemv(L, blob_dev, x, y, xscale=None, y_mode=Y_F32, stream=None):
+    assert L.format == FMT_BITCOS
+    return gemv(L, blob_dev, x, y, xscale, y_mode, stream)
+
+
+def trit5_gemv(L, blob_dev, x, y, xscale=None, y_mode=Y_F32, stream=None):
+    assert L.format == FMT_TRIT5
+    return gemv(L, blob_dev, x, y, xscale, y_mode, stream)
+
+
+def bit2_gemv(L, blob_dev, x, y, xscale=None, y_mode=Y_F32, stream=None):
+    assert L.format == FMT_BIT2
+    return gemv(L, blob_dev, x, y, xscale, y_mode, stream)
+
+
+def describe(L: Layout, m: int = 1, x_dtype: int = X_I8) -> LaunchInfo:
+    info = LaunchInfo()
+    N.check(N.lib().bitcos_describe(ctypes.byref(L), m, x_dtype, ctypes.byref(info)), "bitcos_describe")
+    return info
+
+
+def quantize_activations(x, q, scale, stream=None):
+    """Device int8 quantisation of bf16 activations per group of 128 (see bitcos.h)."""
+    import torch
+    if x.dtype != torch.bfloat16 or q.dtype != torch.int8 or scale.dtype != torch.float32:
+        raise TypeError("x bfloat16, q int8, scale float32")
+    for t in (x, q, scale):
+        if not t.is_cuda or not t.is_contiguous():
+            raise ValueError("contiguous cuda tensors required")
+    m = x.shape[0] if x.dim() == 2 else 1
+    k = x.numel() // m
+    if q.numel() != m * k or scale.numel() != m * (k // 128) or k % 128:
+        raise ValueError("q must be [m, k] and scale [m, k/128], k % 128 == 0")
+    N.check(N.lib().bitcos_quantize_act(ctypes.c_void_p(x.data_ptr()), m, k, ctypes.c_void_p(q.data_ptr()),
+                                        ctypes.c_void_p(scale.data_ptr()), _stream_handle(stream)),
+            "bitcos_quantize_act")
+    return q, scale

@@ -1,0 +1,93 @@
+// Device helpers shared by the three GEMV kernels: wave scans and segmented
+// reductions over 64-wide wavefronts, byte packing, and the per-lane group
+// bookkeeping of the scale epilogue.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace bitcos_dev {
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+constexpr int kWave = 64;
+constexpr int kBlock = 256;  // 4 waves per workgroup
+
+// Inclusive prefix sum over the 64 lanes of a wavefront (DPP row shifts inside
+// each 16-lane row, then row broadcasts 15 and 31 across rows).
+__device__ __forceinline__ int wave_incl_scan(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false);  // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false);  // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false);  // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false);  // row_shr:8
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, false);  // row_bcast:15 -> rows 1, 3
+  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xC, 0xF, false);  // row_bcast:31 -> rows 2, 3
+  return v;
+}
+
+__device__ __forceinline__ int lane63(int v) { return __builtin_amdgcn_readlane(v, 63); }
+
+// Sum over aligned segments of SEG lanes (butterfly; every lane of a segment
+// ends with the same value, summed in the same order).
+template <int SEG>
+__device__ __forceinline__ int seg_sum(int v) {
+#pragma unroll
+  for (int off = SEG / 2; off >= 1; off /= 2) v += __shfl_xor(v, off, kWave);
+  return v;
+}
+
+template <int SEG>
+__device__ __forceinline__ float seg_sum(float v) {
+#pragma unroll
+  for (int off = SEG / 2; off >= 1; off /= 2) v += __shfl_xor(v, off, kWave);
+  return v;
+}
+
+__device__ __forceinline__ uint32_t bytes4(uint32_t b0, uint32_t b1, uint32_t b2, uint32_t b3) {
+  return (b0 & 0xFF) | (b1 & 0xFF) << 8 | (b2 & 0xFF) << 16 | (b3 & 0xFF) << 24;
+}
+
+__device__ __forceinline__ float half_bits_to_float(uint16_t h) {
+  return static_cast<float>(__builtin_bit_cast(_Float16, h));
+}
+
+__device__ __forceinline__ int sdot4(uint32_t a, uint32_t b, int c) {
+  return __builtin_amdgcn_sdot4(static_cast<int>(a), static_cast<int>(b), c, false);
+}
+
+__device__ __forceinline__ float bdot2(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a),
+                                         __builtin_bit_cast(bf16x2_t, b), c, false);
+}
+
+// Running sum at the last unit of every scale group a lane touches.
+//
+// A lane owns units [u0, u0 + PER) of a row (units of UPG per scale group);
+// run[i] is the running accumulator after unit i, constant past the lane's
+// last real unit.  With phase ph = u0 % UPG, group q of the lane ends at unit
+// UPG*q + UPG - 1 - ph (clamped to PER - 1).  NQ = number of groups a lane can
+// touch.  The phase is a run-time lane value; when PER is a multiple of UPG
+// every lane starts on a group boundary and ph is 0.
+template <int PER, int UPG>
+struct GroupEnds {
+  static constexpr bool kAligned = PER % UPG == 0;
+  static constexpr int kNQ = kAligned ? PER / UPG : (PER + 2 * UPG - 2) / UPG;
+
+  template <class T>
+  __device__ __forceinline__ static T pick(const T (&run)[PER], int q, int ph) {
+    if (kAligned) {
+      const int e = UPG * q + UPG - 1;
+      return run[e < PER ? e : PER - 1];
+    }
+    T r = T(0);
+#pragma unroll
+    for (int p = 0; p < UPG; ++p) {
+      int e = UPG * q + UPG - 1 - p;
+      if (e > PER - 1) e = PER - 1;
+      if (e >= 0) r = (ph == p) ? run[e] : r;
+    }
+    return r;
+  }
+};
+
+}  // namespace bitcos_dev

@@ -1,0 +1,64 @@
+// Host-side kernel planning shared by the packers (default unit size) and the
+// GEMV launchers (tile choice).  Pure C++; no HIP types.
+#pragma once
+
+#include <cstdint>
+
+namespace bitcos {
+
+// A GEMV wave covers `rows` = 64 / seg rows per step.  Each row is split over
+// `lanes` <= seg lanes; every lane owns `per_lane` consecutive units of the
+// row (32-weight words for BITCOS, 128-weight blocks for five-trit, 16-weight
+// words for 2-bit).  `seg` is a power of two so a row's partial sums reduce
+// with butterflies inside an aligned lane segment.
+struct Tile {
+  int per_lane = 0;
+  int seg = 0;
+  int rows = 0;
+  int lanes = 0;
+};
+
+// Largest per-lane count that has a compiled kernel, by activation type.
+constexpr int kMaxWordsI8 = 16;    // x in VGPRs: 8 dwords per word
+constexpr int kMaxWordsBf16 = 8;   // x in VGPRs: 16 dwords per word
+
+// Pick the tile that leaves the fewest lanes idle for `units_per_row` units
+// split into chunks of at most `max_per_lane`; ties go to the smaller
+// per-lane count (fewer registers).  Returns false if no tile fits.
+inline bool choose_tile(int units_per_row, int max_per_lane, Tile* t) {
+  double best = -1.0;
+  Tile pick;
+  for (int seg = 64; seg >= 4; seg /= 2) {
+    int per_lane = (units_per_row + seg - 1) / seg;
+    if (per_lane < 1) per_lane = 1;
+    if (per_lane > max_per_lane) continue;
+    int lanes = (units_per_row + per_lane - 1) / per_lane;
+    double util = double(units_per_row) / double(seg * per_lane);
+    bool better = util > best + 1e-12 || (util > best - 1e-12 && per_lane < pick.per_lane);
+    if (better) {
+      best = util;
+      pick.per_lane = per_lane;
+      pick.seg = seg;
+      pick.rows = 64 / seg;
+      pick.lanes = lanes;
+    }
+  }
+  if (best < 0) return false;
+  *t = pick;
+  return true;
+}
+
+// BITCOS tile for (K, activation type): words of 32 weights.
+inline bool bitcos_tile(int k, bool bf16, Tile* t) {
+  return choose_tile(k / 32, bf16 ? kMaxWordsBf16 : kMaxWordsI8, t);
+}
+
+// Default rows per sign offset: one wave step.
+inline int bitcos_default_unit_rows(int n, int k) {
+  Tile t;
+  if (!bitcos_tile(k, false, &t)) return 1;
+  (void)n;
+  return t.rows;
+}
+
+}  // namespace bitcos

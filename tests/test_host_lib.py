@@ -1,0 +1,203 @@
+"""CPU tests of libbitcos.so: exported symbols, host packers vs the oracle, error codes.
+
+The packers are C++ written independently of the oracle; their blobs must be
+byte-identical to the oracle's serialisation of the same (W, scales, unit).
+No GPU work is done here.
+"""
+
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as wl
+
+api = pytest.importorskip("paper_2609_16338_amd.api")
+from paper_2609_16338_amd import _native as N  # noqa: E402
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "bitcos.h")
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\**\s+\**(\w+)\s*\(", text, flags=re.M)))
+
+
+def test_library_loads_and_exports_every_declared_function():
+    names = header_functions()
+    assert "bitcos_gemv" in names and "bit2_unpack" in names and len(names) == 16
+    lib = N.lib()
+    for nm in names:
+        assert hasattr(lib, nm), nm
+    out = subprocess.run(["nm", "-D", "--defined-only", N.LIB_PATH], capture_output=True, text=True).stdout
+    exported = set(re.findall(r"\sT\s(\w+)$", out, flags=re.M))
+    assert set(names) <= exported
+    assert set(names) == set(N.SIGNATURES)
+
+
+def test_version_and_strerror():
+    assert N.lib().bitcos_version() == N.LAYOUT_VERSION
+    for st in (N.OK, N.E_ARG, N.E_VALUE, N.E_SPACE, N.E_HIP, N.E_UNSUPPORTED):
+        assert N.strerror(st)
+    assert N.strerror(-99) == "unknown status"
+
+
+def test_layout_struct_size():
+    assert ctypes.sizeof(N.Layout) == 112
+    assert ctypes.sizeof(N.LaunchInfo) == 32
+
+
+ENC = {N.FMT_BITCOS: O.bitcos_encode, N.FMT_TRIT5: O.trit5_encode, N.FMT_BIT2: O.bit2_encode}
+
+
+def _oracle_blob(fmt, w, sc, group, unit):
+    p = O.bitcos_encode(w, sc, group, unit) if fmt == N.FMT_BITCOS else ENC[fmt](w, sc, group)
+    return p, O.serialize(p)
+
+
+@pytest.mark.parametrize("fmt", [N.FMT_BITCOS, N.FMT_TRIT5, N.FMT_BIT2])
+@pytest.mark.parametrize("z", [0.0, 0.3, 0.42, 0.5, 1.0])
+@pytest.mark.parametrize("group", [128, 0])
+def test_packers_match_oracle_bytes(fmt, z, group):
+    for (n, k) in [(1, 128), (7, 384), (33, 1024), (5, 2560)]:
+        w = wl.ternary(n, k, z, wl.rng_for(40, n, k, int(z * 100)))
+        ns = n * k // 128 if group else 1
+        sc = wl.fp16_uniform((ns,), 0.005, 0.1, wl.rng_for(41, n))
+        unit = 3 if fmt == N.FMT_BITCOS else 0
+        if fmt == N.FMT_BITCOS:
+            L = api.bitcos_plan(w, group, unit)
+        else:
+            L = api.trit5_plan(w, group) if fmt == N.FMT_TRIT5 else api.bit2_plan(w, group)
+        blob = {N.FMT_BITCOS: api.bitcos_pack, N.FMT_TRIT5: api.trit5_pack, N.FMT_BIT2: api.bit2_pack}[fmt](w, sc, L)
+        p, (ob, offs) = _oracle_blob(fmt, w, sc, group, unit)
+        assert bytes(blob) == ob
+        assert L.total_bytes == len(ob)
+        assert L.payload_bits == O.payload_bits(p)
+        assert L.nnz == int(np.count_nonzero(w))
+        idx = [0, 1, 2, 3] if fmt == N.FMT_BITCOS else [0, 3]
+        assert [(L.sec_off[i], L.sec_bytes[i]) for i in idx] == offs
+        unpack = {N.FMT_BITCOS: api.bitcos_unpack, N.FMT_TRIT5: api.trit5_unpack, N.FMT_BIT2: api.bit2_unpack}[fmt]
+        w2, s2 = unpack(L, blob)
+        assert np.array_equal(w2, w) and np.array_equal(s2, sc)
+
+
+def test_bitcos_per_tensor_k_multiple_of_32():
+    w = wl.ternary(5, 96, 0.4, wl.rng_for(42))
+    sc = np.array([0x2E66], np.uint16)
+    L = api.bitcos_plan(w, 0, 2)
+    blob = api.bitcos_pack(w, sc, L)
+    assert bytes(blob) == O.serialize(O.bitcos_encode(w, sc, 0, 2))[0]
+
+
+def test_default_unit_rows_is_positive_and_oracle_agrees():
+    w = wl.ternary(100, 2560, 0.42, wl.rng_for(43))
+    sc = np.array([0x2E66], np.uint16)
+    L = api.bitcos_plan(w, 0, 0)
+    assert L.unit_rows >= 1
+    assert bytes(api.bitcos_pack(w, sc, L)) == O.serialize(O.bitcos_encode(w, sc, 0, L.unit_rows))[0]
+
+
+def test_payload_bits_exact_two_minus_z():
+    n, k = 64, 1024
+    w = wl.ternary(n, k, 0.5, wl.rng_for(44))
+    L = api.bitcos_plan(w, 128, 0)
+    zeros = int(np.count_nonzero(w == 0))
+    assert L.payload_bits == n * k + (n * k - zeros) + 16 * n * (k // 128)
+
+
+def _status(fn, *args):
+    return getattr(N.lib(), fn)(*args)
+
+
+def test_error_codes():
+    L = N.Layout()
+    w = np.zeros((4, 128), np.int8)
+    p = ctypes.c_void_p(w.ctypes.data)
+    assert _status("bitcos_plan", None, 4, 128, 128, 0, ctypes.byref(L)) == N.E_ARG
+    assert _status("bitcos_plan", p, 0, 128, 128, 0, ctypes.byref(L)) == N.E_ARG
+    assert _status("bitcos_plan", p, 4, 100, 128, 0, ctypes.byref(L)) == N.E_ARG    # K % 128
+    assert _status("bitcos_plan", p, 4, 128, 64, 0, ctypes.byref(L)) == N.E_ARG     # bad group
+    assert _status("bitcos_plan", p, 4, 128, 128, -1, ctypes.byref(L)) == N.E_ARG
+    assert _status("trit5_plan", p, 4, 96, 0, ctypes.byref(L)) == N.E_ARG          # blocks of 128
+    bad = w.copy()
+    bad[1, 5] = 3
+    assert _status("bitcos_plan", ctypes.c_void_p(bad.ctypes.data), 4, 128, 128, 0, ctypes.byref(L)) == N.E_VALUE
+    assert _status("bit2_plan", ctypes.c_void_p(bad.ctypes.data), 4, 128, 128, ctypes.byref(L)) == N.E_VALUE
+    # pack: scale checks and capacity
+    L = api.bitcos_plan(w, 128, 0)
+    dst = np.zeros(L.total_bytes, np.uint8)
+    neg = np.full(4, 0xBC00, np.uint16)
+    inf = np.full(4, 0x7C00, np.uint16)
+    ok = np.full(4, 0x3C00, np.uint16)
+    d = ctypes.c_void_p(dst.ctypes.data)
+    assert _status("bitcos_pack", p, ctypes.c_void_p(neg.ctypes.data), ctypes.byref(L), d, dst.nbytes) == N.E_VALUE
+    assert _status("bitcos_pack", p, ctypes.c_void_p(inf.ctypes.data), ctypes.byref(L), d, dst.nbytes) == N.E_VALUE
+    assert _status("bitcos_pack", p, ctypes.c_void_p(ok.ctypes.data), ctypes.byref(L), d, dst.nbytes - 1) == N.E_SPACE
+    # W different from the one planned (more non-zeros) is rejected
+    more = np.ones((4, 128), np.int8)
+    assert _status("bitcos_pack", ctypes.c_void_p(more.ctypes.data), ctypes.c_void_p(ok.ctypes.data),
+                   ctypes.byref(L), d, dst.nbytes) == N.E_VALUE
+    assert _status("bitcos_pack", p, ctypes.c_void_p(ok.ctypes.data), ctypes.byref(L), d, dst.nbytes) == N.OK
+    # wrong version / format
+    L2 = N.Layout.from_buffer_copy(L)
+    L2.version = 99
+    assert _status("bitcos_pack", p, ctypes.c_void_p(ok.ctypes.data), ctypes.byref(L2), d, dst.nbytes) == N.E_ARG
+    L3 = N.Layout.from_buffer_copy(L)
+    L3.format = N.FMT_TRIT5
+    assert _status("bitcos_unpack", ctypes.byref(L3), d, dst.nbytes, p, ctypes.c_void_p(ok.ctypes.data)) == N.E_ARG
+
+
+def test_unpack_detects_corruption():
+    w = wl.ternary(6, 256, 0.4, wl.rng_for(45))
+    sc = wl.fp16_uniform((12,), 0.01, 0.1, wl.rng_for(46))
+    L = api.bitcos_plan(w, 128, 2)
+    blob = api.bitcos_pack(w, sc, L)
+    bad = blob.copy()
+    bad[L.sec_off[N.SEC_OFFSETS] + 4] ^= 1          # a unit offset
+    with pytest.raises(N.BitcosError):
+        api.bitcos_unpack(L, bad)
+    bad = blob.copy()
+    bad[L.sec_off[N.SEC_BITMAP]] ^= 0x10            # one presence bit -> popcount != nnz
+    with pytest.raises(N.BitcosError):
+        api.bitcos_unpack(L, bad)
+    Lt = api.trit5_plan(w, 128)
+    bt = api.trit5_pack(w, sc, Lt)
+    bt[Lt.sec_off[N.SEC_CODES]] = 250               # not a five-trit byte
+    with pytest.raises(N.BitcosError):
+        api.trit5_unpack(Lt, bt)
+    Lb = api.bit2_plan(w, 128)
+    bb = api.bit2_pack(w, sc, Lb)
+    bb[Lb.sec_off[N.SEC_CODES]] |= 3                # code 3
+    with pytest.raises(N.BitcosError):
+        api.bit2_unpack(Lb, bb)
+
+
+def test_gemv_validation_happens_before_any_device_work():
+    # No GPU needed: every one of these is rejected by the host checks.
+    w = wl.ternary(4, 256, 0.4, wl.rng_for(47))
+    L = api.bitcos_plan(w, 128, 0)
+    dummy = ctypes.c_void_p(16)
+    g = N.lib().bitcos_gemv
+    assert g(ctypes.byref(L), None, 1, dummy, N.X_I8, None, dummy, N.Y_F32, None) == N.E_ARG
+    assert g(ctypes.byref(L), dummy, 0, dummy, N.X_I8, None, dummy, N.Y_F32, None) == N.E_ARG
+    assert g(ctypes.byref(L), dummy, 17, dummy, N.X_I8, None, dummy, N.Y_F32, None) == N.E_UNSUPPORTED
+    assert g(ctypes.byref(L), dummy, 1, dummy, 7, None, dummy, N.Y_F32, None) == N.E_ARG
+    assert g(ctypes.byref(L), dummy, 1, dummy, N.X_BF16, None, dummy, N.Y_I32_RAW, None) == N.E_ARG
+    Lt = api.trit5_plan(w, 128)
+    assert N.lib().trit5_gemv(ctypes.byref(L), dummy, 1, dummy, N.X_I8, None, dummy, N.Y_F32, None) == N.E_ARG
+    assert N.lib().bit2_gemv(ctypes.byref(Lt), dummy, 1, dummy, N.X_I8, None, dummy, N.Y_F32, None) == N.E_ARG
+
+
+def test_describe_tiles():
+    for k, per_lane, seg in [(2560, 5, 16), (8192, 4, 64), (6912, 7, 32), (1024, 1, 32), (25600, 13, 64)]:
+        w = np.zeros((8, k), np.int8)
+        L = api.bitcos_plan(w, 128, 0)
+        info = api.describe(L, 1, N.X_I8)
+        assert (info.per_lane, info.seg_lanes) == (per_lane, seg), k
+        assert info.rows_per_step * info.seg_lanes == 64
+        assert info.lanes_used * info.per_lane >= k // 32
