@@ -177,6 +177,33 @@ int bit2_gemv(const bitcos_layout* L, const void* blob_dev, int32_t m, const voi
               int32_t x_dtype, const float* xscale_dev, void* y_dev, int32_t y_mode,
               void* stream);
 
+/* ---- batched GEMVs (one persistent launch for a list of matrices) -------
+ * A decode step runs many GEMVs; launching each on its own leaves the GPU
+ * idle between small kernels.  A batch runs a list of GEMVs of ONE format and
+ * ONE tile (bitcos_describe reports per_lane and seg_lanes) as a single
+ * persistent launch: every wave takes a contiguous range of the list's work
+ * units.  Each GEMV keeps the single-call semantics above (its own x, xscale
+ * and y; y overwritten; m = 1).
+ *
+ * bitcos_batch_bytes: bytes of a batch table for `count` GEMVs (0 if count < 1).
+ *
+ * bitcos_batch_build: fill a host table (table_bytes >= bitcos_batch_bytes)
+ * for `count` GEMVs: layouts[i] (host), blobs_dev[i], x_dev[i], y_dev[i]
+ * (device pointers), xscale_dev NULL or an array of per-GEMV device
+ * pointers (entries may be NULL).  The table records the device pointers:
+ * they must stay valid while the table is in use.  Errors: E_ARG, E_SPACE,
+ * E_UNSUPPORTED (mixed formats or tiles: build one batch per tile).
+ *
+ * bitcos_gemv_batch: copy of the table in device memory (16-byte aligned,
+ * unchanged since built) plus the host table it was copied from; enqueues
+ * one launch on `stream`.  Errors: E_ARG, E_UNSUPPORTED, E_HIP. */
+size_t bitcos_batch_bytes(int32_t count);
+int bitcos_batch_build(int32_t count, const bitcos_layout* layouts, const void* const* blobs_dev,
+                       const void* const* x_dev, const float* const* xscale_dev,
+                       void* const* y_dev, int32_t x_dtype, int32_t y_mode, void* table,
+                       size_t table_bytes);
+int bitcos_gemv_batch(const void* table_host, const void* table_dev, void* stream);
+
 /* ---- activation quantisation --------------------------------------------
  * bitcos_quantize_act: int8 activations for the int8 GEMV path, quantised per
  * group of 128 (Sec. II-C).  The paper does not state the rule; this one is

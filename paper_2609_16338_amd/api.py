@@ -209,3 +209,62 @@ def quantize_activations(x, q, scale, stream=None):
                                         ctypes.c_void_p(scale.data_ptr()), _stream_handle(stream)),
             "bitcos_quantize_act")
     return q, scale
+
+
+class Batch:
+    """A list of GEMVs of one format and tile, run as one persistent launch.
+
+    Holds the host table and its device copy; the device buffers it points to
+    (blobs, activations, outputs) must outlive it.
+    """
+
+    def __init__(self, layouts, blobs_dev, xs, ys, xscales=None, y_mode: int = Y_F32):
+        import torch
+        count = len(layouts)
+        if not (count == len(blobs_dev) == len(xs) == len(ys)) or count < 1:
+            raise ValueError("layouts, blobs, xs and ys must have the same non-zero length")
+        x_dtype = X_I8 if xs[0].dtype == torch.int8 else X_BF16
+        arr = (Layout * count)(*layouts)
+        for L, b, x, y in zip(layouts, blobs_dev, xs, ys):
+            _check_gemv_buffers(L, b, x, y, None, y_mode)
+        if xscales is not None:
+            for L, xs_ in zip(layouts, xscales):
+                if xs_ is not None:
+                    _check_xscale(L, xs_, 1)
+        P = ctypes.c_void_p
+        blobs = (P * count)(*[b.data_ptr() for b in blobs_dev])
+        xp = (P * count)(*[x.data_ptr() for x in xs])
+        yp = (P * count)(*[y.data_ptr() for y in ys])
+        sp = None if xscales is None else (P * count)(*[0 if s is None else s.data_ptr() for s in xscales])
+        nbytes = N.lib().bitcos_batch_bytes(count)
+        self.host = np.zeros(nbytes, dtype=np.uint8)
+        N.check(N.lib().bitcos_batch_build(count, arr, blobs, xp, sp, yp, x_dtype, y_mode,
+                                           _ptr(self.host), nbytes), "bitcos_batch_build")
+        self.dev = torch.from_numpy(self.host).cuda()
+        self.count = count
+        self._keep = (layouts, blobs_dev, xs, ys, xscales)
+
+    def run(self, stream=None):
+        N.check(N.lib().bitcos_gemv_batch(_ptr(self.host), ctypes.c_void_p(self.dev.data_ptr()),
+                                          _stream_handle(stream)), "bitcos_gemv_batch")
+
+
+def _check_gemv_buffers(L, blob_dev, x, y, xscale, y_mode):
+    import torch
+    for t, nm in ((blob_dev, "blob"), (x, "x"), (y, "y")):
+        if not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{nm} must be a contiguous cuda tensor")
+    if blob_dev.dtype != torch.uint8 or blob_dev.numel() < L.total_bytes:
+        raise ValueError("blob_dev must be uint8 with at least total_bytes elements")
+    if x.numel() != L.k or x.dtype not in (torch.int8, torch.bfloat16):
+        raise ValueError("x must be int8 or bfloat16 with k elements")
+    want_y = torch.int32 if y_mode == Y_I32_RAW else torch.float32
+    if y.dtype != want_y or y.numel() != L.n:
+        raise ValueError("y has the wrong dtype or size")
+
+
+def _check_xscale(L, xscale, m):
+    import torch
+    if (not xscale.is_cuda or xscale.dtype != torch.float32 or not xscale.is_contiguous()
+            or xscale.numel() != m * (L.k // 128) or L.k % 128):
+        raise ValueError("xscale must be a contiguous float32 cuda tensor [m, k/128]")

@@ -21,7 +21,11 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libbitcos.so")
 ARCH = "gfx950"
 
-HIP_SOURCES = ["gemv_bitcos.hip", "gemv_fixed.hip", "quantize.hip"]
+HIP_SOURCES = [
+    "gemv_bitcos.hip", "gemv_bitcos_s4.hip", "gemv_bitcos_s8.hip", "gemv_bitcos_s16.hip",
+    "gemv_bitcos_s32.hip", "gemv_bitcos_s64.hip", "gemv_fixed.hip", "fixed_trit5.hip", "fixed_bit2.hip",
+    "batch.hip", "quantize.hip",
+]
 HOST_SOURCES = ["host.cpp"]
 
 COMMON = ["-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-function", f"-I{ROOT}/include"]

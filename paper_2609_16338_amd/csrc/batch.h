@@ -1,0 +1,76 @@
+// Descriptors shared by the host launchers and the persistent GEMV kernels.
+//
+// Every GEMV launch -- one matrix or a whole list of them -- runs as a
+// persistent grid: the matrices' work units (a few rows each) are numbered
+// consecutively across the list, and every wave takes one contiguous range of
+// units, so its activations stay in registers until it crosses into the next
+// matrix and its loads can be issued a step ahead.  A single GEMV passes its
+// one descriptor by value; a batch passes a table in device memory.
+#pragma once
+
+#include <stdint.h>
+
+#include "../../include/bitcos.h"
+
+namespace bitcos {
+
+struct GemvDesc {
+  const void* sec0;         // BITCOS bitmap; five-trit / 2-bit codes
+  const uint32_t* signs;    // BITCOS sign stream
+  const uint32_t* offsets;  // BITCOS per-unit sign offsets
+  const uint16_t* scales;   // fp16 scales
+  const void* x;            // activations [k] (int8 or bf16 bits)
+  const float* xscale;      // NULL or fp32 [k/128]
+  void* y;                  // output [n]
+  int64_t unit_begin;       // first unit of this GEMV in the launch
+  int64_t units;            // units of this GEMV
+  uint32_t nnz;             // BITCOS non-zeros
+  uint32_t last_dword;      // last readable dword of section 0
+  int32_t n;                // rows
+  int32_t upr;              // per-row units: BITCOS / 2-bit words, five-trit blocks
+  int32_t ngroups;          // K / 128 (0 if K % 128 != 0)
+  int32_t unit_rows;        // rows per unit
+  int32_t mode;             // kMode* flags
+  int32_t reserved[7];
+};
+static_assert(sizeof(GemvDesc) == 128, "GemvDesc is 128 bytes");
+
+constexpr int kModeGrouped = 1;  // one scale per (row, 128-group)
+constexpr int kModeXscale = 2;   // per-group activation scales
+constexpr int kModeRaw = 4;      // int32 raw row sums
+
+constexpr uint32_t kBatchMagic = 0x42435342u;  // "BSCB"
+
+// Header of a batch table; `count` descriptors follow at offset 128.
+struct BatchHeader {
+  uint32_t magic;
+  uint32_t version;
+  uint32_t format;
+  int32_t count;
+  int32_t x_dtype;
+  int32_t y_mode;
+  int32_t per_lane;
+  int32_t seg;
+  int64_t total_units;
+  int32_t reserved[22];
+};
+static_assert(sizeof(BatchHeader) == 128, "BatchHeader is 128 bytes");
+
+inline size_t batch_bytes(int32_t count) {
+  return sizeof(BatchHeader) + sizeof(GemvDesc) * static_cast<size_t>(count);
+}
+
+// Persistent launch of one format's kernel over `total_units` units.  With
+// table_dev == nullptr the single descriptor `one` is used.  Defined next to
+// each format's kernels.
+int launch_bitcos(const BatchHeader& h, const GemvDesc* table_dev, const GemvDesc& one, void* stream);
+int launch_fixed(const BatchHeader& h, const GemvDesc* table_dev, const GemvDesc& one, void* stream);
+
+// Tile (per-lane units, lanes per row) the given layout runs with.
+int tile_for(const bitcos_layout* L, int32_t x_dtype, int* per_lane, int* seg, int* rows);
+
+// Fill one descriptor from a layout and device pointers (unit_begin = 0).
+int make_desc(const bitcos_layout* L, const void* blob_dev, const void* x_dev, const float* xscale_dev,
+              void* y_dev, int32_t x_dtype, int32_t y_mode, GemvDesc* d);
+
+}  // namespace bitcos

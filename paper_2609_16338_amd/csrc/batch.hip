@@ -1,0 +1,173 @@
+// Descriptor construction, tile choice and the batch entry points: a list of
+// GEMVs of one format and tile run as one persistent launch.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <string.h>
+
+#include "../../include/bitcos.h"
+#include "batch.h"
+#include "launch_common.h"
+#include "plan.h"
+
+namespace bitcos {
+
+int tile_for(const bitcos_layout* L, int32_t x_dtype, int* per_lane, int* seg, int* rows) {
+  if (x_dtype != BITCOS_X_I8 && x_dtype != BITCOS_X_BF16) return BITCOS_E_ARG;
+  const bool bf16 = x_dtype == BITCOS_X_BF16;
+  Tile t;
+  bool ok;
+  switch (L->format) {
+    case BITCOS_FMT_BITCOS: ok = bitcos_tile(L->k, bf16, &t); break;
+    case BITCOS_FMT_TRIT5: ok = choose_tile(L->k / 128, bf16 ? kMaxBlocksBf16 : kMaxBlocksI8, &t); break;
+    case BITCOS_FMT_BIT2: ok = choose_tile(L->k / 16, bf16 ? kMaxWords2Bf16 : kMaxWords2I8, &t); break;
+    default: return BITCOS_E_ARG;
+  }
+  if (!ok) return BITCOS_E_UNSUPPORTED;
+  *per_lane = t.per_lane;
+  *seg = t.seg;
+  *rows = t.rows;
+  return BITCOS_OK;
+}
+
+static int check_layout(const bitcos_layout* L) {
+  if (!L || L->version != BITCOS_LAYOUT_VERSION) return BITCOS_E_ARG;
+  if (L->n < 1 || L->k < 32 || L->k % 32 || (L->group != 0 && L->group != 128)) return BITCOS_E_ARG;
+  if (L->group == 128 && L->k % 128) return BITCOS_E_ARG;
+  switch (L->format) {
+    case BITCOS_FMT_BITCOS:
+      if (L->unit_rows < 1) return BITCOS_E_ARG;
+      if (L->nnz > 0xFFFFFFFFull) return BITCOS_E_UNSUPPORTED;
+      return BITCOS_OK;
+    case BITCOS_FMT_TRIT5:
+    case BITCOS_FMT_BIT2:
+      return L->k % 128 ? BITCOS_E_ARG : BITCOS_OK;
+    default:
+      return BITCOS_E_ARG;
+  }
+}
+
+int make_desc(const bitcos_layout* L, const void* blob_dev, const void* x_dev, const float* xscale_dev,
+              void* y_dev, int32_t x_dtype, int32_t y_mode, GemvDesc* d) {
+  int st = check_layout(L);
+  if (st) return st;
+  if (x_dtype != BITCOS_X_I8 && x_dtype != BITCOS_X_BF16) return BITCOS_E_ARG;
+  if (y_mode != BITCOS_Y_F32 && y_mode != BITCOS_Y_I32_RAW) return BITCOS_E_ARG;
+  if (y_mode == BITCOS_Y_I32_RAW && x_dtype != BITCOS_X_I8) return BITCOS_E_ARG;
+  if (!blob_dev || !x_dev || !y_dev) return BITCOS_E_ARG;
+  if (xscale_dev && L->k % 128) return BITCOS_E_ARG;
+  int per_lane = 0, seg = 0, rows = 0;
+  st = tile_for(L, x_dtype, &per_lane, &seg, &rows);
+  if (st) return st;
+  memset(d, 0, sizeof(*d));
+  const uint8_t* blob = static_cast<const uint8_t*>(blob_dev);
+  d->sec0 = blob + L->sec_off[0];
+  d->scales = reinterpret_cast<const uint16_t*>(blob + L->sec_off[BITCOS_SEC_SCALES]);
+  d->x = x_dev;
+  d->xscale = xscale_dev;
+  d->y = y_dev;
+  d->n = L->n;
+  d->ngroups = L->k / 128;
+  d->last_dword = static_cast<uint32_t>(L->sec_bytes[0] / 4 - 1);
+  d->mode = (L->group == 128 ? kModeGrouped : 0) | (xscale_dev ? kModeXscale : 0) |
+            (y_mode == BITCOS_Y_I32_RAW ? kModeRaw : 0);
+  if (L->format == BITCOS_FMT_BITCOS) {
+    d->signs = reinterpret_cast<const uint32_t*>(blob + L->sec_off[BITCOS_SEC_SIGNS]);
+    d->offsets = reinterpret_cast<const uint32_t*>(blob + L->sec_off[BITCOS_SEC_OFFSETS]);
+    d->nnz = static_cast<uint32_t>(L->nnz);
+    d->upr = L->k / 32;
+    d->unit_rows = L->unit_rows;
+  } else {
+    d->upr = L->format == BITCOS_FMT_TRIT5 ? L->k / 128 : L->k / 16;
+    d->unit_rows = rows;  // one wave step per unit
+  }
+  d->unit_begin = 0;
+  d->units = (L->n + d->unit_rows - 1) / d->unit_rows;
+  return BITCOS_OK;
+}
+
+static int launch(const BatchHeader& h, const GemvDesc* table_dev, const GemvDesc& one, void* stream) {
+  return h.format == BITCOS_FMT_BITCOS ? launch_bitcos(h, table_dev, one, stream)
+                                       : launch_fixed(h, table_dev, one, stream);
+}
+
+}  // namespace bitcos
+
+extern "C" {
+
+size_t bitcos_batch_bytes(int32_t count) {
+  return count < 1 ? 0 : bitcos::batch_bytes(count);
+}
+
+int bitcos_batch_build(int32_t count, const bitcos_layout* layouts, const void* const* blobs_dev,
+                       const void* const* x_dev, const float* const* xscale_dev, void* const* y_dev,
+                       int32_t x_dtype, int32_t y_mode, void* table, size_t table_bytes) {
+  if (count < 1 || !layouts || !blobs_dev || !x_dev || !y_dev || !table) return BITCOS_E_ARG;
+  if (table_bytes < bitcos::batch_bytes(count)) return BITCOS_E_SPACE;
+  bitcos::BatchHeader h;
+  memset(&h, 0, sizeof(h));
+  h.magic = bitcos::kBatchMagic;
+  h.version = BITCOS_LAYOUT_VERSION;
+  h.format = layouts[0].format;
+  h.count = count;
+  h.x_dtype = x_dtype;
+  h.y_mode = y_mode;
+  bitcos::GemvDesc* descs =
+      reinterpret_cast<bitcos::GemvDesc*>(static_cast<uint8_t*>(table) + sizeof(bitcos::BatchHeader));
+  int64_t units = 0;
+  for (int32_t i = 0; i < count; ++i) {
+    const bitcos_layout* L = &layouts[i];
+    if (L->format != h.format) return BITCOS_E_UNSUPPORTED;
+    int per_lane = 0, seg = 0, rows = 0;
+    int st = bitcos::tile_for(L, x_dtype, &per_lane, &seg, &rows);
+    if (st) return st;
+    if (i == 0) {
+      h.per_lane = per_lane;
+      h.seg = seg;
+    } else if (per_lane != h.per_lane || seg != h.seg) {
+      return BITCOS_E_UNSUPPORTED;  // different tiles: split into one batch per tile
+    }
+    st = bitcos::make_desc(L, blobs_dev[i], x_dev[i], xscale_dev ? xscale_dev[i] : nullptr, y_dev[i],
+                           x_dtype, y_mode, &descs[i]);
+    if (st) return st;
+    descs[i].unit_begin = units;
+    units += descs[i].units;
+  }
+  h.total_units = units;
+  memcpy(table, &h, sizeof(h));
+  return BITCOS_OK;
+}
+
+int bitcos_gemv_batch(const void* table_host, const void* table_dev, void* stream) {
+  if (!table_host || !table_dev) return BITCOS_E_ARG;
+  bitcos::BatchHeader h;
+  memcpy(&h, table_host, sizeof(h));
+  if (h.magic != bitcos::kBatchMagic || h.version != BITCOS_LAYOUT_VERSION || h.count < 1) return BITCOS_E_ARG;
+  if (reinterpret_cast<uintptr_t>(table_dev) % 16) return BITCOS_E_ARG;
+  const bitcos::GemvDesc* descs = reinterpret_cast<const bitcos::GemvDesc*>(
+      static_cast<const uint8_t*>(table_dev) + sizeof(bitcos::BatchHeader));
+  const bitcos::GemvDesc* first = reinterpret_cast<const bitcos::GemvDesc*>(
+      static_cast<const uint8_t*>(table_host) + sizeof(bitcos::BatchHeader));
+  return bitcos::launch(h, descs, *first, stream);
+}
+
+int bitcos_describe(const bitcos_layout* L, int32_t m, int32_t x_dtype, bitcos_launch_info* out) {
+  if (!L || !out) return BITCOS_E_ARG;
+  if (m != 1) return m < 1 ? BITCOS_E_ARG : BITCOS_E_UNSUPPORTED;
+  int st = bitcos::check_layout(L);
+  if (st) return st;
+  int per_lane = 0, seg = 0, rows = 0;
+  st = bitcos::tile_for(L, x_dtype, &per_lane, &seg, &rows);
+  if (st) return st;
+  const int unit_rows = L->format == BITCOS_FMT_BITCOS ? L->unit_rows : rows;
+  const int64_t units = (L->n + unit_rows - 1) / unit_rows;
+  out->per_lane = per_lane;
+  out->seg_lanes = seg;
+  out->rows_per_step = rows;
+  int upr = L->format == BITCOS_FMT_BITCOS ? L->k / 32 : (L->format == BITCOS_FMT_TRIT5 ? L->k / 128 : L->k / 16);
+  out->lanes_used = (upr + per_lane - 1) / per_lane;
+  out->waves = units;          // upper bound: persistent grids use at most the resident waves
+  out->workgroups = (units + 3) / 4;
+  return BITCOS_OK;
+}
+
+}  // extern "C"

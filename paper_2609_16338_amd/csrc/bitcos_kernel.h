@@ -1,0 +1,427 @@
+// BITCOS ternary GEMV for gfx950 (MI355X): y = (S (.) W) x at batch 1.
+//
+// Layout (Sec. II-A of "Breaking the 1.58-bit Barrier for Ternary LLMs"): a
+// presence bitmap with one bit per weight and a sign stream with one bit per
+// non-zero, both in row-major order.  The paper's x86 kernels scatter the
+// compact signs with pdep and its Xe2 kernel with a nibble lookup table
+// (Sec. II-B..D).  CDNA has neither pdep nor the Xe2 block loads, so this
+// kernel is organised around the 64-wide wavefront instead:
+//
+//   * Work split.  A wave step covers R = 64 / SEG consecutive rows; a row is
+//     split over SEG lanes and every lane owns W consecutive 32-weight words
+//     of it, so its activations stay in VGPRs.  Units (groups of rows with a
+//     stored sign offset) of one or many matrices are numbered in one list
+//     and every wave of a persistent grid takes a contiguous range of it.
+//   * Sign cursor.  Rows are consecutive in the sign stream and lanes are in
+//     row-major order, so one wavefront prefix sum of the lanes' non-zero
+//     counts (DPP) gives every lane its entry point; the unit offset stored in
+//     the blob (or the previous step's total) gives the wave's.  Inside a
+//     lane, each word's window starts at the lane's entry plus the popcounts
+//     of its earlier words (Sec. II-D also keeps the address count apart from
+//     the per-group count, to keep the dependent chain short).
+//   * Deposit without pdep.  Per presence byte m, the 8 activations are
+//     compacted onto the present positions with one v_perm_b32 pair (selector
+//     table SEL[m]: byte q = position of the q-th set bit, else zero), and the
+//     next 8 compact sign bits s become +-1 bytes (T[s]); one v_dot4 pair then
+//     gives sum_j (1 - 2 s_j) x_{pos_j}, i.e. Eq. (2) w = p - 2n applied to
+//     the activations instead of the weights.  The cursor moves by
+//     popcount(m).  bf16 activations instead build +-0.5 bf16 weights with
+//     v_perm_b32 from (SELB[m], TH[s]) and use v_dot2_f32_bf16; the factor
+//     0.5 is undone exactly at the end.
+//   * Pipelining.  While step i is decoded, the sign windows of step i+1 and
+//     the presence words (and group scales) of step i+2 are in flight.
+//   * Scales.  int8 dot products accumulate exactly in int32; each scale group
+//     of 128 weights is multiplied once in fp32 (Sec. II-C); with one scale
+//     per tensor the full int32 row sum is multiplied once.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <type_traits>
+#include <utility>
+
+#include "../../include/bitcos.h"
+#include "batch.h"
+#include "device_common.h"
+#include "launch_common.h"
+#include "plan.h"
+
+namespace bitcos_k {
+
+using namespace bitcos_dev;
+using bitcos::GemvDesc;
+using bitcos::kModeGrouped;
+using bitcos::kModeRaw;
+using bitcos::kModeXscale;
+
+struct KernelArgs {
+  const GemvDesc* __restrict__ table;  // batch: descriptor table in device memory
+  int64_t total_units;
+  int32_t count;                       // descriptors in the table
+  int32_t pad;
+  GemvDesc one;                        // single GEMV: its descriptor
+};
+
+// Decode tables, one entry per byte value e.
+//   sel[e]  int8 path: byte q (< popcount e) = bit position of the q-th set
+//           bit of e; other bytes 0x0C (v_perm_b32 writes zero).
+//   tsg[e]  int8 path: byte q = 0xFF if bit q of e is set, else 0x01.
+//   selb[e] bf16 path: 16 selector bytes for 8 bf16 outputs; output b has
+//           low byte 0x0C (zero) and high byte = rank of b in e if present.
+//   tsh[e]  bf16 path: byte q = 0xBF if bit q of e is set, else 0x3F (the
+//           high byte of -0.5 / +0.5).
+template <bool BF16>
+struct Tables;
+template <>
+struct Tables<false> {
+  uint2 sel[256];
+  uint2 tsg[256];
+};
+template <>
+struct Tables<true> {
+  uint4 selb[256];
+  uint2 tsh[256];
+};
+
+template <bool BF16>
+__device__ __forceinline__ void build_tables(Tables<BF16>& t, int e) {
+  uint32_t g[8];
+#pragma unroll
+  for (int b = 0; b < 8; ++b) g[b] = (e >> b & 1) ? (BF16 ? 0xBF : 0xFF) : (BF16 ? 0x3F : 0x01);
+  if constexpr (!BF16) {
+    uint32_t sb[8];
+    int q = 0;
+#pragma unroll
+    for (int b = 0; b < 8; ++b) sb[b] = 0x0C;
+#pragma unroll
+    for (int b = 0; b < 8; ++b)
+      if (e >> b & 1) sb[q++] = b;
+    t.sel[e] = make_uint2(bytes4(sb[0], sb[1], sb[2], sb[3]), bytes4(sb[4], sb[5], sb[6], sb[7]));
+    t.tsg[e] = make_uint2(bytes4(g[0], g[1], g[2], g[3]), bytes4(g[4], g[5], g[6], g[7]));
+  } else {
+    uint32_t hi[8];
+    int r = 0;
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+      hi[b] = (e >> b & 1) ? uint32_t(r) : 0x0Cu;
+      r += e >> b & 1;
+    }
+    t.selb[e] = make_uint4(bytes4(0x0C, hi[0], 0x0C, hi[1]), bytes4(0x0C, hi[2], 0x0C, hi[3]),
+                           bytes4(0x0C, hi[4], 0x0C, hi[5]), bytes4(0x0C, hi[6], 0x0C, hi[7]));
+    t.tsh[e] = make_uint2(bytes4(g[0], g[1], g[2], g[3]), bytes4(g[4], g[5], g[6], g[7]));
+  }
+}
+
+// One 32-weight word, int8 activations: P presence word, S the compact signs
+// of P's non-zeros (bit 0 = first non-zero), x[8] the 32 activations.
+__device__ __forceinline__ int word_i8(uint32_t P, uint32_t S, const uint32_t* x, int acc,
+                                       const Tables<false>& t) {
+  uint32_t r = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t m = (P >> (8 * i)) & 0xFFu;
+    const uint32_t s = (S >> r) & 0xFFu;
+    const uint2 sv = t.sel[m];
+    const uint2 tv = t.tsg[s];
+    const uint32_t c0 = __builtin_amdgcn_perm(x[2 * i + 1], x[2 * i], sv.x);
+    const uint32_t c1 = __builtin_amdgcn_perm(x[2 * i + 1], x[2 * i], sv.y);
+    acc = sdot4(c0, tv.x, acc);
+    acc = sdot4(c1, tv.y, acc);
+    r += __builtin_popcount(m);
+  }
+  return acc;
+}
+
+// Same word with bf16 activations (x[16] = 32 bf16): weights as +-0.5 bf16.
+__device__ __forceinline__ float word_bf16(uint32_t P, uint32_t S, const uint32_t* x, float acc,
+                                           const Tables<true>& t) {
+  uint32_t r = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t m = (P >> (8 * i)) & 0xFFu;
+    const uint32_t s = (S >> r) & 0xFFu;
+    const uint4 sb = t.selb[m];
+    const uint2 th = t.tsh[s];
+    acc = bdot2(__builtin_amdgcn_perm(th.y, th.x, sb.x), x[4 * i + 0], acc);
+    acc = bdot2(__builtin_amdgcn_perm(th.y, th.x, sb.y), x[4 * i + 1], acc);
+    acc = bdot2(__builtin_amdgcn_perm(th.y, th.x, sb.z), x[4 * i + 2], acc);
+    acc = bdot2(__builtin_amdgcn_perm(th.y, th.x, sb.w), x[4 * i + 3], acc);
+    r += __builtin_popcount(m);
+  }
+  return acc;
+}
+
+// The descriptor of GEMV `di`: from the device table (batch launch) or the
+// kernel argument (single GEMV).  Both resolve to scalar loads.
+template <bool TABLE>
+__device__ __forceinline__ const GemvDesc& desc_at(const KernelArgs& a, int di) {
+  if constexpr (TABLE)
+    return a.table[di];
+  else
+    return a.one;
+}
+
+// Wave-uniform description of one step (R rows of one unit of one GEMV).
+struct Step {
+  int di;            // descriptor index
+  int row0;          // first row of the step
+  int row_end;       // end of the unit's rows
+  uint32_t cursor0;  // the unit's sign offset (first step of a unit)
+  bool first;        // first step of its unit
+  bool valid;
+};
+
+// Walks a wave's contiguous unit range [U, Uend) step by step.
+template <int R, bool TABLE>
+struct StepGen {
+  int di;
+  int64_t U, Uend;
+  int t;
+
+  __device__ __forceinline__ Step next(const KernelArgs& a) {
+    Step s;
+    s.valid = false;
+    s.di = 0;
+    s.row0 = 0;
+    s.row_end = 0;
+    s.cursor0 = 0;
+    s.first = false;
+    while (U < Uend) {
+      if constexpr (TABLE) {
+        while (di + 1 < a.count && U >= a.table[di].unit_begin + a.table[di].units) ++di;
+      }
+      const GemvDesc& g = desc_at<TABLE>(a, di);
+      const int64_t u = U - g.unit_begin;
+      const int ur = g.unit_rows;
+      const int r0 = static_cast<int>(u) * ur + t * R;
+      const int rend = min(static_cast<int>(u) * ur + ur, g.n);
+      if (r0 < rend) {
+        s.valid = true;
+        s.di = di;
+        s.row0 = r0;
+        s.row_end = rend;
+        s.first = t == 0;
+        s.cursor0 = s.first ? g.offsets[u] : 0u;
+        if (r0 + R < rend) {
+          ++t;
+        } else {
+          ++U;
+          t = 0;
+        }
+        return s;
+      }
+      ++U;
+      t = 0;
+    }
+    return s;
+  }
+};
+
+template <int W, int SEG, bool BF16, bool TABLE>
+__global__ void __launch_bounds__(kBlock) bitcos_gemv_kernel(const KernelArgs a) {
+  __shared__ Tables<BF16> tab;
+  build_tables<BF16>(tab, threadIdx.x);
+  __syncthreads();
+
+  constexpr int R = kWave / SEG;
+  constexpr int NX = BF16 ? 16 : 8;  // activation dwords per 32-weight word
+  using Acc = typename std::conditional<BF16, float, int>::type;
+  using Ends = GroupEnds<W, 4>;
+  constexpr int NQ = Ends::kNQ;
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(blockIdx.x * (kBlock / kWave) + (threadIdx.x >> 6));
+  const int64_t nwaves = static_cast<int64_t>(gridDim.x) * (kBlock / kWave);
+  const int64_t per = (a.total_units + nwaves - 1) / nwaves;
+  const int64_t U0 = per * wave;
+  const int64_t U1 = min(U0 + per, a.total_units);
+  if (U0 >= U1) return;
+
+  const int rho = lane / SEG;
+  const int j = lane % SEG;
+  const int w0 = j * W;
+  const int ph = Ends::kAligned ? 0 : (w0 & 3);
+  const int g0 = w0 >> 2;
+
+  StepGen<R, TABLE> gen;
+  gen.di = 0;
+  gen.U = U0;
+  gen.Uend = U1;
+  gen.t = 0;
+  if constexpr (TABLE) {  // last descriptor with unit_begin <= U0
+    int lo = 0, hi = a.count;
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (a.table[mid].unit_begin <= U0) lo = mid; else hi = mid;
+    }
+    gen.di = lo;
+  }
+
+  // First stage: presence words and this lane's group scales of step s.
+  auto load_p = [&](const Step& s, uint32_t (&P)[W], uint16_t (&SC)[NQ]) {
+    const GemvDesc& g = desc_at<TABLE>(a, s.di);
+    const int row = s.row0 + rho;
+    const int nwl = max(0, min(W, g.upr - w0));
+    const bool act = s.valid && row < s.row_end && nwl > 0;
+    const uint32_t* bm = static_cast<const uint32_t*>(g.sec0) +
+                         static_cast<size_t>(act ? row : 0) * g.upr + w0;
+#pragma unroll
+    for (int w = 0; w < W; ++w) P[w] = (act && w < nwl) ? bm[w] : 0u;
+    const bool grouped = (g.mode & kModeGrouped) != 0;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const int gi = min(g0 + q, max(g.ngroups - 1, 0));
+      SC[q] = (act && grouped) ? g.scales[static_cast<size_t>(row) * g.ngroups + gi] : uint16_t(0);
+    }
+  };
+
+  // Second stage: wave prefix of the non-zero counts, then the sign windows.
+  uint32_t carry = 0;
+  auto load_s = [&](const Step& s, const uint32_t (&P)[W], uint32_t (&lo)[W], uint32_t (&hi)[W],
+                    uint32_t (&sh)[W]) {
+    const GemvDesc& g = desc_at<TABLE>(a, s.di);
+    int pc[W];
+    int cnt = 0;
+#pragma unroll
+    for (int w = 0; w < W; ++w) {
+      pc[w] = cnt;
+      cnt += __builtin_popcount(P[w]);
+    }
+    const int incl = wave_incl_scan(cnt);
+    const uint32_t cursor = s.first ? s.cursor0 : carry;
+    carry = cursor + static_cast<uint32_t>(lane63(incl));
+    const uint32_t base = cursor + static_cast<uint32_t>(incl - cnt);
+#pragma unroll
+    for (int w = 0; w < W; ++w) {
+      const uint32_t b = min(base + static_cast<uint32_t>(pc[w]), g.nnz);
+      const uint32_t* sp = g.signs + (b >> 5);
+      lo[w] = sp[0];
+      hi[w] = sp[1];
+      sh[w] = b & 31u;
+    }
+  };
+
+  // Lane state of the GEMV whose step is being decoded.
+  int xdi = -1;
+  uint32_t xr[W][NX];
+  float xs[NQ];
+  float tensor_scale = 0.0f;
+  int mode = 0;
+  void* ydst = nullptr;
+
+  Step s1 = gen.next(a);
+  uint32_t P1[W], lo1[W], hi1[W], sh1[W];
+  uint16_t SC1[NQ];
+  load_p(s1, P1, SC1);
+  load_s(s1, P1, lo1, hi1, sh1);
+  Step s2 = gen.next(a);
+  uint32_t P2[W];
+  uint16_t SC2[NQ];
+  load_p(s2, P2, SC2);
+
+  while (s1.valid) {
+    // Rotate: decode s0, scan s1 and fetch its signs, fetch presence of s2.
+    const Step s0 = s1;
+    uint32_t P0[W], lo0[W], hi0[W], sh0[W];
+    uint16_t SC0[NQ];
+#pragma unroll
+    for (int w = 0; w < W; ++w) {
+      P0[w] = P1[w];
+      lo0[w] = lo1[w];
+      hi0[w] = hi1[w];
+      sh0[w] = sh1[w];
+    }
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) SC0[q] = SC1[q];
+    s1 = s2;
+#pragma unroll
+    for (int w = 0; w < W; ++w) P1[w] = P2[w];
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) SC1[q] = SC2[q];
+    if (s1.valid) load_s(s1, P1, lo1, hi1, sh1);
+    s2 = gen.next(a);
+    if (s2.valid) load_p(s2, P2, SC2);
+
+    if (s0.di != xdi) {  // entering another GEMV: its activations and scales
+      xdi = s0.di;
+      const GemvDesc& g = desc_at<TABLE>(a, xdi);
+      const int nwl = max(0, min(W, g.upr - w0));
+      const uint32_t* x32 = static_cast<const uint32_t*>(g.x);
+#pragma unroll
+      for (int w = 0; w < W; ++w)
+#pragma unroll
+        for (int d = 0; d < NX; ++d) xr[w][d] = (w < nwl) ? x32[(w0 + w) * NX + d] : 0u;
+      mode = g.mode;
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const int gi = min(g0 + q, max(g.ngroups - 1, 0));
+        xs[q] = (mode & kModeXscale) ? g.xscale[gi] : 1.0f;
+      }
+      tensor_scale = half_bits_to_float(g.scales[0]);
+      ydst = g.y;
+    }
+
+    const int row = s0.row0 + rho;
+    const bool live = row < s0.row_end;
+    Acc run[W];
+    Acc acc = Acc(0);
+#pragma unroll
+    for (int w = 0; w < W; ++w) {
+      const uint32_t S = __builtin_amdgcn_alignbit(hi0[w], lo0[w], sh0[w]);
+      if constexpr (BF16)
+        acc = word_bf16(P0[w], S, xr[w], acc, tab);
+      else
+        acc = word_i8(P0[w], S, xr[w], acc, tab);
+      run[w] = acc;
+    }
+
+    if (!BF16 && (mode & kModeRaw)) {
+      const int tot = seg_sum<SEG>(static_cast<int>(run[W - 1]));
+      if (j == 0 && live) static_cast<int*>(ydst)[row] = tot;
+      continue;
+    }
+    float part;
+    if (!(mode & (kModeGrouped | kModeXscale))) {
+      // One scale per tensor: reduce the exact row sum, multiply once.
+      if constexpr (BF16) {
+        part = tensor_scale * (2.0f * seg_sum<SEG>(static_cast<float>(run[W - 1])));
+      } else {
+        part = tensor_scale * static_cast<float>(seg_sum<SEG>(static_cast<int>(run[W - 1])));
+      }
+    } else {
+      float f = 0.0f;
+      Acc prev = Acc(0);
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const Acc e = Ends::pick(run, q, ph);
+        const Acc grp = e - prev;
+        prev = e;
+        const float sc = (mode & kModeGrouped) ? half_bits_to_float(SC0[q]) : tensor_scale;
+        f += sc * xs[q] * static_cast<float>(grp);
+      }
+      part = seg_sum<SEG>(BF16 ? 2.0f * f : f);
+    }
+    if (j == 0 && live) static_cast<float*>(ydst)[row] = part;
+  }
+}
+
+using KernelFn = void (*)(const KernelArgs);
+
+template <int SEG, bool BF16, bool TABLE, int... Ws>
+KernelFn pick_w(int w, std::integer_sequence<int, Ws...>) {
+  KernelFn fn = nullptr;
+  ((w == Ws + 1 ? (fn = bitcos_gemv_kernel<Ws + 1, SEG, BF16, TABLE>, 0) : 0), ...);
+  return fn;
+}
+
+// Kernel for (words per lane, bf16?, table?) at a fixed SEG; nullptr if none.
+template <int SEG>
+KernelFn pick_seg(int per_lane, bool bf16, bool table) {
+  auto s8 = std::make_integer_sequence<int, bitcos::kMaxWordsBf16>{};
+  auto s16 = std::make_integer_sequence<int, bitcos::kMaxWordsI8>{};
+  if (bf16) return table ? pick_w<SEG, true, true>(per_lane, s8) : pick_w<SEG, true, false>(per_lane, s8);
+  return table ? pick_w<SEG, false, true>(per_lane, s16) : pick_w<SEG, false, false>(per_lane, s16);
+}
+
+}  // namespace bitcos_k

@@ -1,0 +1,502 @@
+#pragma once
+// Same-GPU baselines for the BITCOS GEMV: five trits per byte (26 bytes per
+// 128 weights, Sec. I of "Breaking the 1.58-bit Barrier for Ternary LLMs")
+// and 2 bits per weight (Table I's 2-bit column).  Both use the BITCOS
+// kernel's work split (a wave step covers 64 / SEG rows; each lane owns
+// consecutive units of a row with its activations in VGPRs) so the three
+// kernels differ only in how they turn bytes into weights.
+//
+//   five-trit  per byte, one LDS lookup gives its five weights as int8 (or
+//              bf16); four lookup tables hold the same five values shifted by
+//              0..3 bytes so that four consecutive bytes (20 weights) OR
+//              together into five dot4 operands without any shuffling.
+//   2-bit      code c = w + 1 sits in bit pairs laid out so that
+//              (word >> 2t) & 0x03030303 are four consecutive codes: one
+//              v_dot4 each, minus the activation sum once per word.  bf16
+//              activations look up four bf16 weights per code byte.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <type_traits>
+#include <utility>
+
+#include "../../include/bitcos.h"
+#include "batch.h"
+#include "device_common.h"
+#include "launch_common.h"
+#include "plan.h"
+
+namespace fixed_k {
+
+using namespace bitcos_dev;
+using bitcos::GemvDesc;
+using bitcos::kModeGrouped;
+using bitcos::kModeRaw;
+using bitcos::kModeXscale;
+
+struct KernelArgs {
+  const GemvDesc* __restrict__ table;  // batch: descriptor table in device memory
+  int64_t total_units;
+  int32_t count;
+  int32_t pad;
+  GemvDesc one;                        // single GEMV: its descriptor
+};
+
+template <bool TABLE>
+__device__ __forceinline__ const GemvDesc& desc_at(const KernelArgs& a, int di) {
+  if constexpr (TABLE)
+    return a.table[di];
+  else
+    return a.one;
+}
+
+// Row range and descriptor of one unit (= one wave step of R rows).
+struct Step {
+  int di;
+  int row0;
+  int row_end;
+  bool valid;
+};
+
+template <int R, bool TABLE>
+struct StepGen {
+  int di;
+  int64_t U, Uend;
+
+  __device__ __forceinline__ Step next(const KernelArgs& a) {
+    Step s;
+    s.valid = U < Uend;
+    s.di = di;
+    s.row0 = 0;
+    s.row_end = 0;
+    if (!s.valid) return s;
+    if constexpr (TABLE) {
+      while (di + 1 < a.count && U >= a.table[di].unit_begin + a.table[di].units) ++di;
+    }
+    const GemvDesc& g = desc_at<TABLE>(a, di);
+    const int64_t u = U - g.unit_begin;
+    s.di = di;
+    s.row0 = static_cast<int>(u) * R;
+    s.row_end = min(s.row0 + R, g.n);
+    ++U;
+    return s;
+  }
+};
+
+// The wave's contiguous unit range of a persistent launch; returns false if empty.
+template <int R, bool TABLE>
+__device__ __forceinline__ bool wave_range(const KernelArgs& a, StepGen<R, TABLE>& gen) {
+  const int wave = __builtin_amdgcn_readfirstlane(blockIdx.x * (kBlock / kWave) + (threadIdx.x >> 6));
+  const int64_t nwaves = static_cast<int64_t>(gridDim.x) * (kBlock / kWave);
+  const int64_t per = (a.total_units + nwaves - 1) / nwaves;
+  gen.U = per * wave;
+  gen.Uend = min(gen.U + per, a.total_units);
+  gen.di = 0;
+  if constexpr (TABLE) {
+    int lo = 0, hi = a.count;
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (a.table[mid].unit_begin <= gen.U) lo = mid; else hi = mid;
+    }
+    gen.di = lo;
+  }
+  return gen.U < gen.Uend;
+}
+
+// Common epilogue: reduce the lane partials of one row and store.  SC holds
+// the row's group scales for the lane's groups (fp16 bits, grouped mode).
+template <int SEG, bool BF16, int PER, int UPG, class Acc>
+__device__ __forceinline__ void finish_row(int mode, void* ydst, const Acc (&run)[PER], int row,
+                                           bool live, int j, int ph, const float* xs,
+                                           const uint16_t* SC, float tensor_scale) {
+  using Ends = GroupEnds<PER, UPG>;
+  if (!BF16 && (mode & kModeRaw)) {
+    const int tot = seg_sum<SEG>(static_cast<int>(run[PER - 1]));
+    if (j == 0 && live) static_cast<int*>(ydst)[row] = tot;
+    return;
+  }
+  float part;
+  if (!(mode & (kModeGrouped | kModeXscale))) {
+    if constexpr (BF16) {
+      part = tensor_scale * seg_sum<SEG>(static_cast<float>(run[PER - 1]));
+    } else {
+      part = tensor_scale * static_cast<float>(seg_sum<SEG>(static_cast<int>(run[PER - 1])));
+    }
+  } else {
+    float f = 0.0f;
+    Acc prev = Acc(0);
+#pragma unroll
+    for (int q = 0; q < Ends::kNQ; ++q) {
+      const Acc e = Ends::pick(run, q, ph);
+      const Acc grp = e - prev;
+      prev = e;
+      const float s = (mode & kModeGrouped) ? half_bits_to_float(SC[q]) : tensor_scale;
+      f += s * xs[q] * static_cast<float>(grp);
+    }
+    part = seg_sum<SEG>(f);
+  }
+  if (j == 0 && live) static_cast<float*>(ydst)[row] = part;
+}
+
+// The lane's group scales for one row (grouped mode), else zeros.
+template <int NQ>
+__device__ __forceinline__ void load_row_scales(const GemvDesc& g, int row, bool act, int g0,
+                                                uint16_t (&SC)[NQ]) {
+  const bool grouped = (g.mode & kModeGrouped) != 0;
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    const int gi = min(g0 + q, max(g.ngroups - 1, 0));
+    SC[q] = (act && grouped) ? g.scales[static_cast<size_t>(row) * g.ngroups + gi] : uint16_t(0);
+  }
+}
+
+template <int NQ>
+__device__ __forceinline__ void load_xscales(const GemvDesc& g, int g0, float (&xs)[NQ]) {
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    const int gi = min(g0 + q, max(g.ngroups - 1, 0));
+    xs[q] = (g.mode & kModeXscale) ? g.xscale[gi] : 1.0f;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Five-trit
+// ---------------------------------------------------------------------------
+
+// tab[p][v]: the five weights of byte value v (digits base 3, digit = w + 1,
+// first weight in the lowest digit) as int8, placed at byte offset p of an
+// 8-byte entry.  Values 243..255 are not produced by the packer: all zero.
+struct Trit5TablesI8 {
+  uint2 t[4][256];
+};
+// bf16 variant: five bf16 weights starting at element 0 or 1 of a 16-byte
+// entry (an even byte of a block starts on a dword, an odd one half-way in).
+struct Trit5TablesBf16 {
+  uint4 t[2][256];
+};
+
+__device__ __forceinline__ void trit5_digits(int v, int (&w)[5]) {
+  bool ok = v < 243;
+#pragma unroll
+  for (int t = 0; t < 5; ++t) {
+    w[t] = ok ? (v % 3) - 1 : 0;
+    v /= 3;
+  }
+}
+
+__device__ __forceinline__ void build_trit5_i8(Trit5TablesI8& tb, int v) {
+  int w[5];
+  trit5_digits(v, w);
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    uint32_t b[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+    for (int t = 0; t < 5; ++t) b[p + t] = uint32_t(w[t]) & 0xFF;
+    tb.t[p][v] = make_uint2(bytes4(b[0], b[1], b[2], b[3]), bytes4(b[4], b[5], b[6], b[7]));
+  }
+}
+
+__device__ __forceinline__ void build_trit5_bf16(Trit5TablesBf16& tb, int v) {
+  int w[5];
+  trit5_digits(v, w);
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    uint32_t h[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+    for (int t = 0; t < 5; ++t) h[p + t] = w[t] == 0 ? 0u : (w[t] > 0 ? 0x3F80u : 0xBF80u);
+    tb.t[p][v] = make_uint4(h[0] | h[1] << 16, h[2] | h[3] << 16, h[4] | h[5] << 16, h[6] | h[7] << 16);
+  }
+}
+
+// Byte i of the lane's aligned code stream A.
+template <int NA>
+__device__ __forceinline__ uint32_t code_byte(const uint32_t (&A)[NA], int i) {
+  return (A[i >> 2] >> (8 * (i & 3))) & 0xFFu;
+}
+
+template <int BK, int SEG, bool BF16, bool TABLE>
+__global__ void __launch_bounds__(kBlock) trit5_gemv_kernel(const KernelArgs a) {
+  using Tables = typename std::conditional<BF16, Trit5TablesBf16, Trit5TablesI8>::type;
+  __shared__ Tables tab;
+  if constexpr (BF16)
+    build_trit5_bf16(tab, threadIdx.x);
+  else
+    build_trit5_i8(tab, threadIdx.x);
+  __syncthreads();
+
+  constexpr int R = kWave / SEG;
+  constexpr int NX = BF16 ? 64 : 32;             // activation dwords per block
+  constexpr int ND = (2 + 26 * BK + 3) / 4 + 1;  // code dwords loaded per lane
+  using Acc = typename std::conditional<BF16, float, int>::type;
+
+  StepGen<R, TABLE> gen;
+  if (!wave_range(a, gen)) return;
+  const int lane = threadIdx.x & 63;
+  const int rho = lane / SEG;
+  const int j = lane % SEG;
+  const int b0 = j * BK;
+
+  auto load_c = [&](const Step& s, uint32_t (&cw)[ND], uint32_t& o, uint16_t (&SC)[BK]) {
+    const GemvDesc& g = desc_at<TABLE>(a, s.di);
+    const int row = s.row0 + rho;
+    const int nbl = max(0, min(BK, g.upr - b0));
+    const bool act = s.valid && row < s.row_end && nbl > 0;
+    const uint64_t start = (static_cast<uint64_t>(act ? row : 0) * g.upr + b0) * 26u;
+    o = static_cast<uint32_t>(start & 3u);
+    const uint32_t d0 = static_cast<uint32_t>(start >> 2);
+    const uint32_t* c32 = static_cast<const uint32_t*>(g.sec0);
+#pragma unroll
+    for (int d = 0; d < ND; ++d) cw[d] = act ? c32[min(d0 + d, g.last_dword)] : 0u;
+    load_row_scales<BK>(g, row, act, b0, SC);
+  };
+
+  int xdi = -1;
+  uint32_t xr[BK][NX];
+  float xs[BK];
+  float tensor_scale = 0.0f;
+  int mode = 0;
+  void* ydst = nullptr;
+
+  Step s1 = gen.next(a);
+  uint32_t cw1[ND], o1;
+  uint16_t SC1[BK];
+  load_c(s1, cw1, o1, SC1);
+  while (s1.valid) {
+    const Step s0 = s1;
+    uint32_t A[ND - 1];
+#pragma unroll
+    for (int d = 0; d < ND - 1; ++d) A[d] = __builtin_amdgcn_alignbyte(cw1[d + 1], cw1[d], o1);
+    uint16_t SC0[BK];
+#pragma unroll
+    for (int t = 0; t < BK; ++t) SC0[t] = SC1[t];
+    s1 = gen.next(a);
+    if (s1.valid) load_c(s1, cw1, o1, SC1);
+
+    if (s0.di != xdi) {
+      xdi = s0.di;
+      const GemvDesc& g = desc_at<TABLE>(a, xdi);
+      const int nbl = max(0, min(BK, g.upr - b0));
+      const uint32_t* x32 = static_cast<const uint32_t*>(g.x);
+#pragma unroll
+      for (int t = 0; t < BK; ++t)
+#pragma unroll
+        for (int d = 0; d < NX; ++d) xr[t][d] = (t < nbl) ? x32[(b0 + t) * NX + d] : 0u;
+      load_xscales<BK>(g, b0, xs);
+      tensor_scale = half_bits_to_float(g.scales[0]);
+      mode = g.mode;
+      ydst = g.y;
+    }
+
+    const int row = s0.row0 + rho;
+    const bool live = row < s0.row_end;
+    Acc run[BK];
+    Acc acc = Acc(0);
+#pragma unroll
+    for (int t = 0; t < BK; ++t) {
+      const uint32_t* x = xr[t];
+      if constexpr (!BF16) {
+#pragma unroll
+        for (int c = 0; c < 6; ++c) {
+          const uint2 e0 = tab.t[0][code_byte(A, 26 * t + 4 * c + 0)];
+          const uint2 e1 = tab.t[1][code_byte(A, 26 * t + 4 * c + 1)];
+          const uint2 e2 = tab.t[2][code_byte(A, 26 * t + 4 * c + 2)];
+          const uint2 e3 = tab.t[3][code_byte(A, 26 * t + 4 * c + 3)];
+          acc = sdot4(e0.x, x[5 * c + 0], acc);
+          acc = sdot4(e0.y | e1.x, x[5 * c + 1], acc);
+          acc = sdot4(e1.y | e2.x, x[5 * c + 2], acc);
+          acc = sdot4(e2.y | e3.x, x[5 * c + 3], acc);
+          acc = sdot4(e3.y, x[5 * c + 4], acc);
+        }
+        const uint2 e0 = tab.t[0][code_byte(A, 26 * t + 24)];
+        const uint2 e1 = tab.t[1][code_byte(A, 26 * t + 25)];
+        acc = sdot4(e0.x, x[30], acc);
+        acc = sdot4(e0.y | e1.x, x[31], acc);
+      } else {
+#pragma unroll
+        for (int c = 0; c < 13; ++c) {
+          const uint4 e0 = tab.t[0][code_byte(A, 26 * t + 2 * c + 0)];
+          const uint4 e1 = tab.t[1][code_byte(A, 26 * t + 2 * c + 1)];
+          acc = bdot2(e0.x, x[5 * c + 0], acc);
+          acc = bdot2(e0.y, x[5 * c + 1], acc);
+          acc = bdot2(e0.z | e1.x, x[5 * c + 2], acc);
+          acc = bdot2(e1.y, x[5 * c + 3], acc);
+          if (c < 12) acc = bdot2(e1.z, x[5 * c + 4], acc);  // weights 128, 129 do not exist
+        }
+      }
+      run[t] = acc;
+    }
+    finish_row<SEG, BF16, BK, 1>(mode, ydst, run, row, live, j, 0, xs, SC0, tensor_scale);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// 2-bit
+// ---------------------------------------------------------------------------
+
+// bf16 table: code byte v holds weights k0+b, k0+4+b, k0+8+b, k0+12+b (bit
+// pairs 0..3); entry = those four weights as bf16, pairs (t0,t1), (t2,t3).
+struct Bit2TablesBf16 {
+  uint2 t[256];
+};
+
+__device__ __forceinline__ void build_bit2_bf16(Bit2TablesBf16& tb, int v) {
+  uint32_t h[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    int c = (v >> (2 * t)) & 3;
+    h[t] = c == 0 ? 0xBF80u : (c == 2 ? 0x3F80u : 0u);
+  }
+  tb.t[v] = make_uint2(h[0] | h[1] << 16, h[2] | h[3] << 16);
+}
+
+template <int WB, int SEG, bool BF16, bool TABLE>
+__global__ void __launch_bounds__(kBlock) bit2_gemv_kernel(const KernelArgs a) {
+  __shared__ Bit2TablesBf16 tab;
+  if constexpr (BF16) {
+    build_bit2_bf16(tab, threadIdx.x);
+    __syncthreads();
+  }
+
+  constexpr int R = kWave / SEG;
+  constexpr int NX = BF16 ? 8 : 4;  // activation dwords per 16-weight word
+  using Acc = typename std::conditional<BF16, float, int>::type;
+  using Ends = GroupEnds<WB, 8>;
+  constexpr int NQ = Ends::kNQ;
+
+  StepGen<R, TABLE> gen;
+  if (!wave_range(a, gen)) return;
+  const int lane = threadIdx.x & 63;
+  const int rho = lane / SEG;
+  const int j = lane % SEG;
+  const int u0 = j * WB;
+  const int ph = Ends::kAligned ? 0 : (u0 & 7);
+  const int g0 = u0 >> 3;
+
+  auto load_c = [&](const Step& s, uint32_t (&cw)[WB], uint16_t (&SC)[NQ]) {
+    const GemvDesc& g = desc_at<TABLE>(a, s.di);
+    const int row = s.row0 + rho;
+    const int nul = max(0, min(WB, g.upr - u0));
+    const bool act = s.valid && row < s.row_end && nul > 0;
+    const uint32_t* cp = static_cast<const uint32_t*>(g.sec0) + static_cast<size_t>(act ? row : 0) * g.upr + u0;
+#pragma unroll
+    for (int w = 0; w < WB; ++w) cw[w] = (act && w < nul) ? cp[w] : 0x55555555u;  // code 1 = weight 0
+    load_row_scales<NQ>(g, row, act, g0, SC);
+  };
+
+  // int8: x in natural order; the per-word activation sum corrects c = w + 1.
+  // bf16: x permuted to match the code bytes: dword 2b + h holds
+  // (x[k0 + 8h + b], x[k0 + 8h + 4 + b]).
+  int xdi = -1;
+  uint32_t xr[WB][NX];
+  int xsum[WB];
+  float xs[NQ];
+  float tensor_scale = 0.0f;
+  int mode = 0;
+  void* ydst = nullptr;
+
+  Step s1 = gen.next(a);
+  uint32_t cw1[WB];
+  uint16_t SC1[NQ];
+  load_c(s1, cw1, SC1);
+  while (s1.valid) {
+    const Step s0 = s1;
+    uint32_t cw0[WB];
+    uint16_t SC0[NQ];
+#pragma unroll
+    for (int w = 0; w < WB; ++w) cw0[w] = cw1[w];
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) SC0[q] = SC1[q];
+    s1 = gen.next(a);
+    if (s1.valid) load_c(s1, cw1, SC1);
+
+    if (s0.di != xdi) {
+      xdi = s0.di;
+      const GemvDesc& g = desc_at<TABLE>(a, xdi);
+      const int nul = max(0, min(WB, g.upr - u0));
+#pragma unroll
+      for (int w = 0; w < WB; ++w) {
+        const bool ok = w < nul;
+        if constexpr (!BF16) {
+          const uint32_t* x32 = static_cast<const uint32_t*>(g.x) + (u0 + w) * 4;
+          int s = 0;
+#pragma unroll
+          for (int d = 0; d < 4; ++d) {
+            xr[w][d] = ok ? x32[d] : 0u;
+            s = sdot4(xr[w][d], 0x01010101u, s);
+          }
+          xsum[w] = s;
+        } else {
+          const uint16_t* x16 = static_cast<const uint16_t*>(g.x) + (u0 + w) * 16;
+#pragma unroll
+          for (int b = 0; b < 4; ++b)
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+              xr[w][2 * b + h] = ok ? (uint32_t(x16[8 * h + b]) | uint32_t(x16[8 * h + 4 + b]) << 16) : 0u;
+          xsum[w] = 0;
+        }
+      }
+      load_xscales<NQ>(g, g0, xs);
+      tensor_scale = half_bits_to_float(g.scales[0]);
+      mode = g.mode;
+      ydst = g.y;
+    }
+
+    const int row = s0.row0 + rho;
+    const bool live = row < s0.row_end;
+    Acc run[WB];
+    Acc acc = Acc(0);
+#pragma unroll
+    for (int w = 0; w < WB; ++w) {
+      const uint32_t c = cw0[w];
+      if constexpr (!BF16) {
+        acc -= xsum[w];
+        acc = sdot4(c & 0x03030303u, xr[w][0], acc);
+        acc = sdot4((c >> 2) & 0x03030303u, xr[w][1], acc);
+        acc = sdot4((c >> 4) & 0x03030303u, xr[w][2], acc);
+        acc = sdot4((c >> 6) & 0x03030303u, xr[w][3], acc);
+      } else {
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          const uint2 e = tab.t[(c >> (8 * b)) & 0xFFu];
+          acc = bdot2(e.x, xr[w][2 * b + 0], acc);
+          acc = bdot2(e.y, xr[w][2 * b + 1], acc);
+        }
+      }
+      run[w] = acc;
+    }
+    finish_row<SEG, BF16, WB, 8>(mode, ydst, run, row, live, j, ph, xs, SC0, tensor_scale);
+  }
+}
+
+using KernelFn = void (*)(const KernelArgs);
+
+template <int P, int SEG, bool BF16, bool TABLE>
+struct Trit5K {
+  static constexpr KernelFn fn = trit5_gemv_kernel<P, SEG, BF16, TABLE>;
+};
+template <int P, int SEG, bool BF16, bool TABLE>
+struct Bit2K {
+  static constexpr KernelFn fn = bit2_gemv_kernel<P, SEG, BF16, TABLE>;
+};
+
+template <template <int, int, bool, bool> class K, int SEG, bool BF16, bool TABLE, int... Ps>
+KernelFn pick_p(int p, std::integer_sequence<int, Ps...>) {
+  KernelFn fn = nullptr;
+  ((p == Ps + 1 ? (fn = K<Ps + 1, SEG, BF16, TABLE>::fn, 0) : 0), ...);
+  return fn;
+}
+
+template <template <int, int, bool, bool> class K, int MAX, bool BF16, bool TABLE>
+KernelFn pick_kernel(int per_lane, int seg) {
+  auto seq = std::make_integer_sequence<int, MAX>{};
+  switch (seg) {
+    case 4: return pick_p<K, 4, BF16, TABLE>(per_lane, seq);
+    case 8: return pick_p<K, 8, BF16, TABLE>(per_lane, seq);
+    case 16: return pick_p<K, 16, BF16, TABLE>(per_lane, seq);
+    case 32: return pick_p<K, 32, BF16, TABLE>(per_lane, seq);
+    case 64: return pick_p<K, 64, BF16, TABLE>(per_lane, seq);
+    default: return nullptr;
+  }
+}
+
+}  // namespace fixed_k

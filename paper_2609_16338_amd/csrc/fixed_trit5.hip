@@ -1,0 +1,12 @@
+// Five-trit GEMV kernel instantiations (kernels in fixed_kernel.h).
+#include "fixed_kernel.h"
+
+namespace fixed_k {
+KernelFn pick_trit5(int per_lane, int seg, bool bf16, bool table) {
+  if (bf16)
+    return table ? pick_kernel<Trit5K, bitcos::kMaxBlocksBf16, true, true>(per_lane, seg)
+                 : pick_kernel<Trit5K, bitcos::kMaxBlocksBf16, true, false>(per_lane, seg);
+  return table ? pick_kernel<Trit5K, bitcos::kMaxBlocksI8, false, true>(per_lane, seg)
+               : pick_kernel<Trit5K, bitcos::kMaxBlocksI8, false, false>(per_lane, seg);
+}
+}  // namespace fixed_k

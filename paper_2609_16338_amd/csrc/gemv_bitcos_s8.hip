@@ -1,0 +1,7 @@
+// BITCOS GEMV kernels with 8 lanes per row segment (one file per segment
+// width so the instantiations compile in parallel).
+#include "bitcos_kernel.h"
+
+namespace bitcos_k {
+KernelFn pick_seg_8(int per_lane, bool bf16, bool table) { return pick_seg<8>(per_lane, bf16, table); }
+}  // namespace bitcos_k

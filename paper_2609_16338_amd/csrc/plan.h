@@ -19,8 +19,12 @@ struct Tile {
 };
 
 // Largest per-lane count that has a compiled kernel, by activation type.
-constexpr int kMaxWordsI8 = 16;    // x in VGPRs: 8 dwords per word
-constexpr int kMaxWordsBf16 = 8;   // x in VGPRs: 16 dwords per word
+constexpr int kMaxWordsI8 = 16;    // BITCOS: x in VGPRs, 8 dwords per 32-weight word
+constexpr int kMaxWordsBf16 = 8;   // BITCOS: 16 dwords per word
+constexpr int kMaxBlocksI8 = 5;    // five-trit: 32 dwords per 128-weight block
+constexpr int kMaxBlocksBf16 = 2;  // five-trit: 64 dwords per block
+constexpr int kMaxWords2I8 = 32;   // 2-bit: 4 dwords per 16-weight word
+constexpr int kMaxWords2Bf16 = 16; // 2-bit: 8 dwords per word
 
 // Pick the tile that leaves the fewest lanes idle for `units_per_row` units
 // split into chunks of at most `max_per_lane`; ties go to the smaller

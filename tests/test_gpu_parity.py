@@ -345,3 +345,81 @@ def test_quantize_activations_bit_exact(m, k):
     qr, ar = O.quantize_activations(xb)
     assert np.array_equal(a.cpu().numpy().view(np.uint32), ar.view(np.uint32))
     assert np.array_equal(q.cpu().numpy(), qr)
+
+
+# ---------------------------------------------------------------------------
+# Batched launch: a list of GEMVs of one tile as one persistent kernel
+# ---------------------------------------------------------------------------
+
+def _batch_case(fmt, kind, group, with_xscale=False):
+    # Matrices of one K (same tile): different row counts, densities and seeds.
+    k = 2560
+    specs = [(64, 0.42), (7, 0.0), (640, 0.5), (33, 1.0), (301, 0.467)]
+    mats, blobs, xs, ys, scs, refs, bounds, layouts, xss = [], [], [], [], [], [], [], [], []
+    for i, (n, z) in enumerate(specs):
+        w, sc = inputs(n, k, z, group, 200 + i)
+        if kind == "int8":
+            x = wl.act_int8(1, k, wl.rng_for(201, i))
+            xs_np = None
+            if with_xscale:
+                xb = wl.act_bf16(1, k, wl.rng_for(202, i))
+                x, xs_np = O.quantize_activations(xb)
+            ref = O.dense_gemv(w, sc, group, x, xs_np)
+            bound = group_bound(w, sc, group, x, xs_np)
+        else:
+            x = wl.act_bf16(1, k, wl.rng_for(203, i))
+            xs_np = None
+            ref = O.dense_gemv(w, sc, group, x, x_is_bf16_bits=True)
+            bound = bf16_bound(w, sc, group, x)
+        L, blob = api.plan_and_pack(fmt, w, sc, group)
+        layouts.append(L)
+        blobs.append(torch.from_numpy(blob).cuda())
+        xs.append(to_dev_x(x, kind).reshape(-1))
+        xss.append(None if xs_np is None else torch.from_numpy(np.ascontiguousarray(xs_np, np.float32)).cuda())
+        ys.append(torch.full((w.shape[0],), -7.0, dtype=torch.float32, device="cuda"))
+        refs.append(ref)
+        bounds.append(bound)
+    say("batch", FMT_NAME[fmt], kind, f"group={group}", "xscale" if with_xscale else "")
+    b = api.Batch(layouts, blobs, xs, ys, xss if with_xscale else None)
+    b.run()
+    torch.cuda.synchronize()
+    for y, ref, bound, kind_ in zip(ys, refs, bounds, [kind] * len(ys)):
+        got = y.cpu().numpy()[None]
+        if kind == "bf16":
+            check_bf16(got, ref, bound)
+        elif group == 0 and not with_xscale:
+            assert np.array_equal(got, ref)
+        else:
+            check_grouped(got, ref, bound)
+    # a second run gives identical bits
+    first = [y.cpu().numpy().copy() for y in ys]
+    b.run()
+    torch.cuda.synchronize()
+    for y, f in zip(ys, first):
+        assert np.array_equal(y.cpu().numpy().view(np.uint32), f.view(np.uint32))
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("kind,group,xscale", [("int8", 128, False), ("int8", 0, False), ("int8", 0, True),
+                                               ("bf16", 0, False), ("bf16", 128, False)])
+def test_batch_matches_oracle(fmt, kind, group, xscale):
+    _batch_case(fmt, kind, group, xscale)
+
+
+def test_batch_rejects_mixed_tiles_and_formats():
+    w1, s1 = inputs(8, 2560, 0.4, 128, 300)
+    w2, s2 = inputs(8, 6912, 0.4, 128, 301)
+    L1, b1 = api.plan_and_pack(N.FMT_BITCOS, w1, s1, 128)
+    L2, b2 = api.plan_and_pack(N.FMT_BITCOS, w2, s2, 128)
+    L3, b3 = api.plan_and_pack(N.FMT_TRIT5, w1, s1, 128)
+    dev = lambda a: torch.from_numpy(a).cuda()  # noqa: E731
+    x1 = torch.zeros(2560, dtype=torch.int8, device="cuda")
+    x2 = torch.zeros(6912, dtype=torch.int8, device="cuda")
+    y1 = torch.zeros(8, dtype=torch.float32, device="cuda")
+    y2 = torch.zeros(8, dtype=torch.float32, device="cuda")
+    with pytest.raises(N.BitcosError) as e:
+        api.Batch([L1, L2], [dev(b1), dev(b2)], [x1, x2], [y1, y2])
+    assert e.value.status == N.E_UNSUPPORTED
+    with pytest.raises(N.BitcosError) as e:
+        api.Batch([L1, L3], [dev(b1), dev(b3)], [x1, x1], [y1, y2])
+    assert e.value.status == N.E_UNSUPPORTED
