@@ -31,7 +31,11 @@ struct GemvDesc {
   int32_t ngroups;          // K / 128 (0 if K % 128 != 0)
   int32_t unit_rows;        // rows per unit
   int32_t mode;             // kMode* flags
-  int32_t reserved[7];
+  uint32_t sec0_bytes;      // bytes of section 0
+  uint32_t signs_bytes;     // bytes of the sign stream (with its zero tail)
+  uint32_t scales_bytes;    // bytes of the scales
+  uint32_t x_bytes;         // bytes of the activations
+  int32_t reserved[3];
 };
 static_assert(sizeof(GemvDesc) == 128, "GemvDesc is 128 bytes");
 

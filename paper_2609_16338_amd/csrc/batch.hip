@@ -68,10 +68,15 @@ int make_desc(const bitcos_layout* L, const void* blob_dev, const void* x_dev, c
   d->n = L->n;
   d->ngroups = L->k / 128;
   d->last_dword = static_cast<uint32_t>(L->sec_bytes[0] / 4 - 1);
+  if (L->sec_bytes[0] >= 0x80000000ull || L->total_bytes >= 0x80000000ull) return BITCOS_E_UNSUPPORTED;
+  d->sec0_bytes = static_cast<uint32_t>(L->sec_bytes[0]);
+  d->scales_bytes = static_cast<uint32_t>(L->sec_bytes[BITCOS_SEC_SCALES]);
+  d->x_bytes = static_cast<uint32_t>(L->k) * (x_dtype == BITCOS_X_BF16 ? 2u : 1u);
   d->mode = (L->group == 128 ? kModeGrouped : 0) | (xscale_dev ? kModeXscale : 0) |
             (y_mode == BITCOS_Y_I32_RAW ? kModeRaw : 0);
   if (L->format == BITCOS_FMT_BITCOS) {
     d->signs = reinterpret_cast<const uint32_t*>(blob + L->sec_off[BITCOS_SEC_SIGNS]);
+    d->signs_bytes = static_cast<uint32_t>(L->sec_bytes[BITCOS_SEC_SIGNS]);
     d->offsets = reinterpret_cast<const uint32_t*>(blob + L->sec_off[BITCOS_SEC_OFFSETS]);
     d->nnz = static_cast<uint32_t>(L->nnz);
     d->upr = L->k / 32;

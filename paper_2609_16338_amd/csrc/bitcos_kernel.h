@@ -63,7 +63,10 @@ struct KernelArgs {
   GemvDesc one;                        // single GEMV: its descriptor
 };
 
-// Decode tables, one entry per byte value e.
+// Decode tables, one entry per byte value e, each kept in NC copies: lane l
+// reads copy l % NC, and copy c of every entry sits c entries past the start
+// of the entry's group of copies, so lanes that read the same cycle hit
+// different LDS banks whatever keys they look up.
 //   sel[e]  int8 path: byte q (< popcount e) = bit position of the q-th set
 //           bit of e; other bytes 0x0C (v_perm_b32 writes zero).
 //   tsg[e]  int8 path: byte q = 0xFF if bit q of e is set, else 0x01.
@@ -72,23 +75,33 @@ struct KernelArgs {
 //   tsh[e]  bf16 path: byte q = 0xBF if bit q of e is set, else 0x3F (the
 //           high byte of -0.5 / +0.5).
 template <bool BF16>
-struct Tables;
-template <>
-struct Tables<false> {
-  uint2 sel[256];
-  uint2 tsg[256];
-};
-template <>
-struct Tables<true> {
-  uint4 selb[256];
-  uint2 tsh[256];
+struct Cfg {
+  static constexpr int kThreads = BF16 ? 256 : 512;  // workgroup size
+  static constexpr int kCopies = BF16 ? 8 : 16;      // table copies
 };
 
 template <bool BF16>
-__device__ __forceinline__ void build_tables(Tables<BF16>& t, int e) {
+struct Tables;
+template <>
+struct Tables<false> {
+  uint2 sel[256 * Cfg<false>::kCopies];
+  uint2 tsg[256 * Cfg<false>::kCopies];
+};
+template <>
+struct Tables<true> {
+  uint4 selb[256 * Cfg<true>::kCopies];
+  uint2 tsh[256 * Cfg<true>::kCopies];
+};
+
+template <bool BF16>
+__device__ __forceinline__ void build_tables(Tables<BF16>& t, int tid) {
+  constexpr int NC = Cfg<BF16>::kCopies;
+  constexpr int PASSES = 256 * NC / Cfg<BF16>::kThreads;
+  const int e = tid & 255;
   uint32_t g[8];
 #pragma unroll
   for (int b = 0; b < 8; ++b) g[b] = (e >> b & 1) ? (BF16 ? 0xBF : 0xFF) : (BF16 ? 0x3F : 0x01);
+  const uint2 gv = make_uint2(bytes4(g[0], g[1], g[2], g[3]), bytes4(g[4], g[5], g[6], g[7]));
   if constexpr (!BF16) {
     uint32_t sb[8];
     int q = 0;
@@ -97,8 +110,13 @@ __device__ __forceinline__ void build_tables(Tables<BF16>& t, int e) {
 #pragma unroll
     for (int b = 0; b < 8; ++b)
       if (e >> b & 1) sb[q++] = b;
-    t.sel[e] = make_uint2(bytes4(sb[0], sb[1], sb[2], sb[3]), bytes4(sb[4], sb[5], sb[6], sb[7]));
-    t.tsg[e] = make_uint2(bytes4(g[0], g[1], g[2], g[3]), bytes4(g[4], g[5], g[6], g[7]));
+    const uint2 sv = make_uint2(bytes4(sb[0], sb[1], sb[2], sb[3]), bytes4(sb[4], sb[5], sb[6], sb[7]));
+#pragma unroll
+    for (int p = 0; p < PASSES; ++p) {
+      const int c = (tid >> 8) + p * (Cfg<BF16>::kThreads / 256);
+      t.sel[e * NC + c] = sv;
+      t.tsg[e * NC + c] = gv;
+    }
   } else {
     uint32_t hi[8];
     int r = 0;
@@ -107,23 +125,30 @@ __device__ __forceinline__ void build_tables(Tables<BF16>& t, int e) {
       hi[b] = (e >> b & 1) ? uint32_t(r) : 0x0Cu;
       r += e >> b & 1;
     }
-    t.selb[e] = make_uint4(bytes4(0x0C, hi[0], 0x0C, hi[1]), bytes4(0x0C, hi[2], 0x0C, hi[3]),
-                           bytes4(0x0C, hi[4], 0x0C, hi[5]), bytes4(0x0C, hi[6], 0x0C, hi[7]));
-    t.tsh[e] = make_uint2(bytes4(g[0], g[1], g[2], g[3]), bytes4(g[4], g[5], g[6], g[7]));
+    const uint4 sv = make_uint4(bytes4(0x0C, hi[0], 0x0C, hi[1]), bytes4(0x0C, hi[2], 0x0C, hi[3]),
+                                bytes4(0x0C, hi[4], 0x0C, hi[5]), bytes4(0x0C, hi[6], 0x0C, hi[7]));
+#pragma unroll
+    for (int p = 0; p < PASSES; ++p) {
+      const int c = (tid >> 8) + p * (Cfg<BF16>::kThreads / 256);
+      t.selb[e * NC + c] = sv;
+      t.tsh[e * NC + c] = gv;
+    }
   }
 }
 
 // One 32-weight word, int8 activations: P presence word, S the compact signs
-// of P's non-zeros (bit 0 = first non-zero), x[8] the 32 activations.
+// of P's non-zeros (bit 0 = first non-zero), x[8] the 32 activations; `cp`
+// is this lane's table copy.
 __device__ __forceinline__ int word_i8(uint32_t P, uint32_t S, const uint32_t* x, int acc,
-                                       const Tables<false>& t) {
+                                       const Tables<false>& t, int cp) {
+  constexpr int NC = Cfg<false>::kCopies;
   uint32_t r = 0;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const uint32_t m = (P >> (8 * i)) & 0xFFu;
     const uint32_t s = (S >> r) & 0xFFu;
-    const uint2 sv = t.sel[m];
-    const uint2 tv = t.tsg[s];
+    const uint2 sv = t.sel[m * NC + cp];
+    const uint2 tv = t.tsg[s * NC + cp];
     const uint32_t c0 = __builtin_amdgcn_perm(x[2 * i + 1], x[2 * i], sv.x);
     const uint32_t c1 = __builtin_amdgcn_perm(x[2 * i + 1], x[2 * i], sv.y);
     acc = sdot4(c0, tv.x, acc);
@@ -135,14 +160,15 @@ __device__ __forceinline__ int word_i8(uint32_t P, uint32_t S, const uint32_t* x
 
 // Same word with bf16 activations (x[16] = 32 bf16): weights as +-0.5 bf16.
 __device__ __forceinline__ float word_bf16(uint32_t P, uint32_t S, const uint32_t* x, float acc,
-                                           const Tables<true>& t) {
+                                           const Tables<true>& t, int cp) {
+  constexpr int NC = Cfg<true>::kCopies;
   uint32_t r = 0;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const uint32_t m = (P >> (8 * i)) & 0xFFu;
     const uint32_t s = (S >> r) & 0xFFu;
-    const uint4 sb = t.selb[m];
-    const uint2 th = t.tsh[s];
+    const uint4 sb = t.selb[m * NC + cp];
+    const uint2 th = t.tsh[s * NC + cp];
     acc = bdot2(__builtin_amdgcn_perm(th.y, th.x, sb.x), x[4 * i + 0], acc);
     acc = bdot2(__builtin_amdgcn_perm(th.y, th.x, sb.y), x[4 * i + 1], acc);
     acc = bdot2(__builtin_amdgcn_perm(th.y, th.x, sb.z), x[4 * i + 2], acc);
@@ -152,14 +178,16 @@ __device__ __forceinline__ float word_bf16(uint32_t P, uint32_t S, const uint32_
   return acc;
 }
 
-// The descriptor of GEMV `di`: from the device table (batch launch) or the
-// kernel argument (single GEMV).  Both resolve to scalar loads.
+// The descriptor of GEMV `di` (a wave-uniform index): from the device table
+// (batch launch) or the kernel argument (single GEMV); scalar loads either way.
+typedef const __attribute__((address_space(4))) GemvDesc CDesc;
+
 template <bool TABLE>
-__device__ __forceinline__ const GemvDesc& desc_at(const KernelArgs& a, int di) {
+__device__ __forceinline__ decltype(auto) desc_at(const KernelArgs& a, int di) {
   if constexpr (TABLE)
-    return a.table[di];
+    return static_cast<CDesc&>(((CDesc*)a.table)[__builtin_amdgcn_readfirstlane(di)]);
   else
-    return a.one;
+    return static_cast<const GemvDesc&>(a.one);
 }
 
 // Wave-uniform description of one step (R rows of one unit of one GEMV).
@@ -189,9 +217,10 @@ struct StepGen {
     s.first = false;
     while (U < Uend) {
       if constexpr (TABLE) {
-        while (di + 1 < a.count && U >= a.table[di].unit_begin + a.table[di].units) ++di;
+        while (di + 1 < a.count && U >= desc_at<TABLE>(a, di).unit_begin + desc_at<TABLE>(a, di).units) ++di;
+        di = __builtin_amdgcn_readfirstlane(di);
       }
-      const GemvDesc& g = desc_at<TABLE>(a, di);
+      const auto& g = desc_at<TABLE>(a, di);
       const int64_t u = U - g.unit_begin;
       const int ur = g.unit_rows;
       const int r0 = static_cast<int>(u) * ur + t * R;
@@ -202,7 +231,7 @@ struct StepGen {
         s.row0 = r0;
         s.row_end = rend;
         s.first = t == 0;
-        s.cursor0 = s.first ? g.offsets[u] : 0u;
+        s.cursor0 = s.first ? cp_u32(g.offsets)[u] : 0u;
         if (r0 + R < rend) {
           ++t;
         } else {
@@ -219,20 +248,21 @@ struct StepGen {
 };
 
 template <int W, int SEG, bool BF16, bool TABLE>
-__global__ void __launch_bounds__(kBlock) bitcos_gemv_kernel(const KernelArgs a) {
+__global__ void __launch_bounds__(Cfg<BF16>::kThreads) bitcos_gemv_kernel(const KernelArgs a) {
   __shared__ Tables<BF16> tab;
   build_tables<BF16>(tab, threadIdx.x);
   __syncthreads();
 
   constexpr int R = kWave / SEG;
   constexpr int NX = BF16 ? 16 : 8;  // activation dwords per 32-weight word
+  constexpr int WPB = Cfg<BF16>::kThreads / kWave;
   using Acc = typename std::conditional<BF16, float, int>::type;
   using Ends = GroupEnds<W, 4>;
   constexpr int NQ = Ends::kNQ;
 
   const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(blockIdx.x * (kBlock / kWave) + (threadIdx.x >> 6));
-  const int64_t nwaves = static_cast<int64_t>(gridDim.x) * (kBlock / kWave);
+  const int wave = __builtin_amdgcn_readfirstlane(blockIdx.x * WPB + (threadIdx.x >> 6));
+  const int64_t nwaves = static_cast<int64_t>(gridDim.x) * WPB;
   const int64_t per = (a.total_units + nwaves - 1) / nwaves;
   const int64_t U0 = per * wave;
   const int64_t U1 = min(U0 + per, a.total_units);
@@ -243,6 +273,7 @@ __global__ void __launch_bounds__(kBlock) bitcos_gemv_kernel(const KernelArgs a)
   const int w0 = j * W;
   const int ph = Ends::kAligned ? 0 : (w0 & 3);
   const int g0 = w0 >> 2;
+  const int cp = lane & (Cfg<BF16>::kCopies - 1);
 
   StepGen<R, TABLE> gen;
   gen.di = 0;
@@ -253,26 +284,31 @@ __global__ void __launch_bounds__(kBlock) bitcos_gemv_kernel(const KernelArgs a)
     int lo = 0, hi = a.count;
     while (hi - lo > 1) {
       const int mid = (lo + hi) >> 1;
-      if (a.table[mid].unit_begin <= U0) lo = mid; else hi = mid;
+      if (((CDesc*)a.table)[mid].unit_begin <= U0) lo = mid; else hi = mid;
     }
-    gen.di = lo;
+    gen.di = __builtin_amdgcn_readfirstlane(lo);
   }
 
   // First stage: presence words and this lane's group scales of step s.
   auto load_p = [&](const Step& s, uint32_t (&P)[W], uint16_t (&SC)[NQ]) {
-    const GemvDesc& g = desc_at<TABLE>(a, s.di);
+    const auto& g = desc_at<TABLE>(a, s.di);
     const int row = s.row0 + rho;
     const int nwl = max(0, min(W, g.upr - w0));
-    const bool act = s.valid && row < s.row_end && nwl > 0;
-    const uint32_t* bm = static_cast<const uint32_t*>(g.sec0) +
-                         static_cast<size_t>(act ? row : 0) * g.upr + w0;
+    const bool act = s.valid && row < s.row_end;
+    const rsrc_t rb = make_rsrc(g.sec0, g.sec0_bytes);
+    const uint32_t off = act ? (static_cast<uint32_t>(row) * g.upr + w0) * 4u : kOOB;
 #pragma unroll
-    for (int w = 0; w < W; ++w) P[w] = (act && w < nwl) ? bm[w] : 0u;
+    for (int w = 0; w < W; ++w) {
+      const uint32_t v = ld32(rb, off + 4u * w);
+      P[w] = w < nwl ? v : 0u;
+    }
+    const rsrc_t rs = make_rsrc(g.scales, g.scales_bytes);
     const bool grouped = (g.mode & kModeGrouped) != 0;
+    const uint32_t soff = (act && grouped) ? static_cast<uint32_t>(row) * g.ngroups * 2u : kOOB;
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
       const int gi = min(g0 + q, max(g.ngroups - 1, 0));
-      SC[q] = (act && grouped) ? g.scales[static_cast<size_t>(row) * g.ngroups + gi] : uint16_t(0);
+      SC[q] = ld16(rs, soff + 2u * gi);
     }
   };
 
@@ -280,7 +316,7 @@ __global__ void __launch_bounds__(kBlock) bitcos_gemv_kernel(const KernelArgs a)
   uint32_t carry = 0;
   auto load_s = [&](const Step& s, const uint32_t (&P)[W], uint32_t (&lo)[W], uint32_t (&hi)[W],
                     uint32_t (&sh)[W]) {
-    const GemvDesc& g = desc_at<TABLE>(a, s.di);
+    const auto& g = desc_at<TABLE>(a, s.di);
     int pc[W];
     int cnt = 0;
 #pragma unroll
@@ -292,12 +328,13 @@ __global__ void __launch_bounds__(kBlock) bitcos_gemv_kernel(const KernelArgs a)
     const uint32_t cursor = s.first ? s.cursor0 : carry;
     carry = cursor + static_cast<uint32_t>(lane63(incl));
     const uint32_t base = cursor + static_cast<uint32_t>(incl - cnt);
+    const rsrc_t rg = make_rsrc(g.signs, g.signs_bytes);
 #pragma unroll
     for (int w = 0; w < W; ++w) {
-      const uint32_t b = min(base + static_cast<uint32_t>(pc[w]), g.nnz);
-      const uint32_t* sp = g.signs + (b >> 5);
-      lo[w] = sp[0];
-      hi[w] = sp[1];
+      const uint32_t b = base + static_cast<uint32_t>(pc[w]);
+      const uint32_t off = (b >> 5) * 4u;
+      lo[w] = ld32(rg, off);
+      hi[w] = ld32(rg, off + 4u);
       sh[w] = b & 31u;
     }
   };
@@ -345,20 +382,22 @@ __global__ void __launch_bounds__(kBlock) bitcos_gemv_kernel(const KernelArgs a)
 
     if (s0.di != xdi) {  // entering another GEMV: its activations and scales
       xdi = s0.di;
-      const GemvDesc& g = desc_at<TABLE>(a, xdi);
+      const auto& g = desc_at<TABLE>(a, xdi);
       const int nwl = max(0, min(W, g.upr - w0));
-      const uint32_t* x32 = static_cast<const uint32_t*>(g.x);
+      const rsrc_t rx = make_rsrc(g.x, g.x_bytes);
 #pragma unroll
-      for (int w = 0; w < W; ++w)
+      for (int w = 0; w < W; ++w) {
+        const uint32_t off = w < nwl ? static_cast<uint32_t>(w0 + w) * NX * 4u : kOOB;
 #pragma unroll
-        for (int d = 0; d < NX; ++d) xr[w][d] = (w < nwl) ? x32[(w0 + w) * NX + d] : 0u;
+        for (int d = 0; d < NX; ++d) xr[w][d] = ld32(rx, off + 4u * d);
+      }
       mode = g.mode;
 #pragma unroll
       for (int q = 0; q < NQ; ++q) {
         const int gi = min(g0 + q, max(g.ngroups - 1, 0));
-        xs[q] = (mode & kModeXscale) ? g.xscale[gi] : 1.0f;
+        xs[q] = (mode & kModeXscale) ? gp_f32(g.xscale)[gi] : 1.0f;
       }
-      tensor_scale = half_bits_to_float(g.scales[0]);
+      tensor_scale = half_bits_to_float(gp_u16(g.scales)[0]);
       ydst = g.y;
     }
 
@@ -370,15 +409,15 @@ __global__ void __launch_bounds__(kBlock) bitcos_gemv_kernel(const KernelArgs a)
     for (int w = 0; w < W; ++w) {
       const uint32_t S = __builtin_amdgcn_alignbit(hi0[w], lo0[w], sh0[w]);
       if constexpr (BF16)
-        acc = word_bf16(P0[w], S, xr[w], acc, tab);
+        acc = word_bf16(P0[w], S, xr[w], acc, tab, cp);
       else
-        acc = word_i8(P0[w], S, xr[w], acc, tab);
+        acc = word_i8(P0[w], S, xr[w], acc, tab, cp);
       run[w] = acc;
     }
 
     if (!BF16 && (mode & kModeRaw)) {
       const int tot = seg_sum<SEG>(static_cast<int>(run[W - 1]));
-      if (j == 0 && live) static_cast<int*>(ydst)[row] = tot;
+      if (j == 0 && live) gp_i32_out(ydst)[row] = tot;
       continue;
     }
     float part;
@@ -402,7 +441,7 @@ __global__ void __launch_bounds__(kBlock) bitcos_gemv_kernel(const KernelArgs a)
       }
       part = seg_sum<SEG>(BF16 ? 2.0f * f : f);
     }
-    if (j == 0 && live) static_cast<float*>(ydst)[row] = part;
+    if (j == 0 && live) gp_f32_out(ydst)[row] = part;
   }
 }
 

@@ -10,6 +10,45 @@ namespace bitcos_dev {
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 
+// Pointers into global memory.  Descriptor fields are generic pointers; using
+// them through these types makes every access a global_* instruction (a flat
+// access would also count against the LDS counter and serialise the
+// prefetched loads with the table lookups).
+typedef const __attribute__((address_space(1))) uint32_t* g_u32;
+typedef const __attribute__((address_space(1))) uint16_t* g_u16;
+typedef const __attribute__((address_space(1))) float* g_f32;
+typedef __attribute__((address_space(1))) int* g_i32_out;
+typedef __attribute__((address_space(1))) float* g_f32_out;
+
+// Read-only for the whole kernel (descriptor tables, unit offsets): the
+// constant address space lets these wave-uniform reads go through the scalar
+// cache into SGPRs.
+typedef const __attribute__((address_space(4))) uint32_t* c_u32;
+__device__ __forceinline__ c_u32 cp_u32(const void* p) { return (c_u32)p; }
+
+__device__ __forceinline__ g_u32 gp_u32(const void* p) { return (g_u32)p; }
+__device__ __forceinline__ g_u16 gp_u16(const void* p) { return (g_u16)p; }
+__device__ __forceinline__ g_f32 gp_f32(const void* p) { return (g_f32)p; }
+__device__ __forceinline__ g_i32_out gp_i32_out(void* p) { return (g_i32_out)p; }
+__device__ __forceinline__ g_f32_out gp_f32_out(void* p) { return (g_f32_out)p; }
+
+// Buffer resources: a load through one checks its byte offset against the
+// resource size and returns 0 past it, so lanes with nothing to read (a
+// ragged last lane, rows past the end) pass kOOB and need no branch.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr uint32_t kOOB = 0x80000000u;  // past every section (sections are < 2 GiB)
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0),
+                                           static_cast<int>(bytes), 0x00020000);
+}
+__device__ __forceinline__ uint32_t ld32(rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+}
+__device__ __forceinline__ uint16_t ld16(rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
+}
+
 constexpr int kWave = 64;
 constexpr int kBlock = 256;  // 4 waves per workgroup
 

@@ -42,12 +42,14 @@ struct KernelArgs {
   GemvDesc one;                        // single GEMV: its descriptor
 };
 
+typedef const __attribute__((address_space(4))) GemvDesc CDesc;
+
 template <bool TABLE>
-__device__ __forceinline__ const GemvDesc& desc_at(const KernelArgs& a, int di) {
+__device__ __forceinline__ decltype(auto) desc_at(const KernelArgs& a, int di) {
   if constexpr (TABLE)
-    return a.table[di];
+    return static_cast<CDesc&>(((CDesc*)a.table)[__builtin_amdgcn_readfirstlane(di)]);
   else
-    return a.one;
+    return static_cast<const GemvDesc&>(a.one);
 }
 
 // Row range and descriptor of one unit (= one wave step of R rows).
@@ -71,9 +73,10 @@ struct StepGen {
     s.row_end = 0;
     if (!s.valid) return s;
     if constexpr (TABLE) {
-      while (di + 1 < a.count && U >= a.table[di].unit_begin + a.table[di].units) ++di;
+      while (di + 1 < a.count && U >= desc_at<TABLE>(a, di).unit_begin + desc_at<TABLE>(a, di).units) ++di;
+      di = __builtin_amdgcn_readfirstlane(di);
     }
-    const GemvDesc& g = desc_at<TABLE>(a, di);
+    const auto& g = desc_at<TABLE>(a, di);
     const int64_t u = U - g.unit_begin;
     s.di = di;
     s.row0 = static_cast<int>(u) * R;
@@ -96,9 +99,9 @@ __device__ __forceinline__ bool wave_range(const KernelArgs& a, StepGen<R, TABLE
     int lo = 0, hi = a.count;
     while (hi - lo > 1) {
       const int mid = (lo + hi) >> 1;
-      if (a.table[mid].unit_begin <= gen.U) lo = mid; else hi = mid;
+      if (((CDesc*)a.table)[mid].unit_begin <= gen.U) lo = mid; else hi = mid;
     }
-    gen.di = lo;
+    gen.di = __builtin_amdgcn_readfirstlane(lo);
   }
   return gen.U < gen.Uend;
 }
@@ -112,7 +115,7 @@ __device__ __forceinline__ void finish_row(int mode, void* ydst, const Acc (&run
   using Ends = GroupEnds<PER, UPG>;
   if (!BF16 && (mode & kModeRaw)) {
     const int tot = seg_sum<SEG>(static_cast<int>(run[PER - 1]));
-    if (j == 0 && live) static_cast<int*>(ydst)[row] = tot;
+    if (j == 0 && live) gp_i32_out(ydst)[row] = tot;
     return;
   }
   float part;
@@ -135,27 +138,29 @@ __device__ __forceinline__ void finish_row(int mode, void* ydst, const Acc (&run
     }
     part = seg_sum<SEG>(f);
   }
-  if (j == 0 && live) static_cast<float*>(ydst)[row] = part;
+  if (j == 0 && live) gp_f32_out(ydst)[row] = part;
 }
 
 // The lane's group scales for one row (grouped mode), else zeros.
-template <int NQ>
-__device__ __forceinline__ void load_row_scales(const GemvDesc& g, int row, bool act, int g0,
+template <int NQ, class G>
+__device__ __forceinline__ void load_row_scales(const G& g, int row, bool act, int g0,
                                                 uint16_t (&SC)[NQ]) {
   const bool grouped = (g.mode & kModeGrouped) != 0;
+  const rsrc_t rs = make_rsrc(g.scales, g.scales_bytes);
+  const uint32_t soff = (act && grouped) ? static_cast<uint32_t>(row) * g.ngroups * 2u : kOOB;
 #pragma unroll
   for (int q = 0; q < NQ; ++q) {
     const int gi = min(g0 + q, max(g.ngroups - 1, 0));
-    SC[q] = (act && grouped) ? g.scales[static_cast<size_t>(row) * g.ngroups + gi] : uint16_t(0);
+    SC[q] = ld16(rs, soff + 2u * gi);
   }
 }
 
-template <int NQ>
-__device__ __forceinline__ void load_xscales(const GemvDesc& g, int g0, float (&xs)[NQ]) {
+template <int NQ, class G>
+__device__ __forceinline__ void load_xscales(const G& g, int g0, float (&xs)[NQ]) {
 #pragma unroll
   for (int q = 0; q < NQ; ++q) {
     const int gi = min(g0 + q, max(g.ngroups - 1, 0));
-    xs[q] = (g.mode & kModeXscale) ? g.xscale[gi] : 1.0f;
+    xs[q] = (g.mode & kModeXscale) ? gp_f32(g.xscale)[gi] : 1.0f;
   }
 }
 
@@ -237,16 +242,16 @@ __global__ void __launch_bounds__(kBlock) trit5_gemv_kernel(const KernelArgs a) 
   const int b0 = j * BK;
 
   auto load_c = [&](const Step& s, uint32_t (&cw)[ND], uint32_t& o, uint16_t (&SC)[BK]) {
-    const GemvDesc& g = desc_at<TABLE>(a, s.di);
+    const auto& g = desc_at<TABLE>(a, s.di);
     const int row = s.row0 + rho;
     const int nbl = max(0, min(BK, g.upr - b0));
     const bool act = s.valid && row < s.row_end && nbl > 0;
-    const uint64_t start = (static_cast<uint64_t>(act ? row : 0) * g.upr + b0) * 26u;
-    o = static_cast<uint32_t>(start & 3u);
-    const uint32_t d0 = static_cast<uint32_t>(start >> 2);
-    const uint32_t* c32 = static_cast<const uint32_t*>(g.sec0);
+    const uint32_t start = (static_cast<uint32_t>(act ? row : 0) * g.upr + b0) * 26u;
+    o = start & 3u;
+    const uint32_t off = act ? (start & ~3u) : kOOB;
+    const rsrc_t rc = make_rsrc(g.sec0, g.sec0_bytes);
 #pragma unroll
-    for (int d = 0; d < ND; ++d) cw[d] = act ? c32[min(d0 + d, g.last_dword)] : 0u;
+    for (int d = 0; d < ND; ++d) cw[d] = ld32(rc, off + 4u * d);
     load_row_scales<BK>(g, row, act, b0, SC);
   };
 
@@ -274,15 +279,17 @@ __global__ void __launch_bounds__(kBlock) trit5_gemv_kernel(const KernelArgs a) 
 
     if (s0.di != xdi) {
       xdi = s0.di;
-      const GemvDesc& g = desc_at<TABLE>(a, xdi);
+      const auto& g = desc_at<TABLE>(a, xdi);
       const int nbl = max(0, min(BK, g.upr - b0));
-      const uint32_t* x32 = static_cast<const uint32_t*>(g.x);
+      const rsrc_t rx = make_rsrc(g.x, g.x_bytes);
 #pragma unroll
-      for (int t = 0; t < BK; ++t)
+      for (int t = 0; t < BK; ++t) {
+        const uint32_t off = t < nbl ? static_cast<uint32_t>(b0 + t) * NX * 4u : kOOB;
 #pragma unroll
-        for (int d = 0; d < NX; ++d) xr[t][d] = (t < nbl) ? x32[(b0 + t) * NX + d] : 0u;
+        for (int d = 0; d < NX; ++d) xr[t][d] = ld32(rx, off + 4u * d);
+      }
       load_xscales<BK>(g, b0, xs);
-      tensor_scale = half_bits_to_float(g.scales[0]);
+      tensor_scale = half_bits_to_float(gp_u16(g.scales)[0]);
       mode = g.mode;
       ydst = g.y;
     }
@@ -373,13 +380,17 @@ __global__ void __launch_bounds__(kBlock) bit2_gemv_kernel(const KernelArgs a) {
   const int g0 = u0 >> 3;
 
   auto load_c = [&](const Step& s, uint32_t (&cw)[WB], uint16_t (&SC)[NQ]) {
-    const GemvDesc& g = desc_at<TABLE>(a, s.di);
+    const auto& g = desc_at<TABLE>(a, s.di);
     const int row = s.row0 + rho;
     const int nul = max(0, min(WB, g.upr - u0));
     const bool act = s.valid && row < s.row_end && nul > 0;
-    const uint32_t* cp = static_cast<const uint32_t*>(g.sec0) + static_cast<size_t>(act ? row : 0) * g.upr + u0;
+    const rsrc_t rc = make_rsrc(g.sec0, g.sec0_bytes);
+    const uint32_t off = act ? (static_cast<uint32_t>(row) * g.upr + u0) * 4u : kOOB;
 #pragma unroll
-    for (int w = 0; w < WB; ++w) cw[w] = (act && w < nul) ? cp[w] : 0x55555555u;  // code 1 = weight 0
+    for (int w = 0; w < WB; ++w) {
+      const uint32_t v = ld32(rc, off + 4u * w);
+      cw[w] = w < nul ? v : 0x55555555u;  // code 1 = weight 0
+    }
     load_row_scales<NQ>(g, row, act, g0, SC);
   };
 
@@ -411,32 +422,34 @@ __global__ void __launch_bounds__(kBlock) bit2_gemv_kernel(const KernelArgs a) {
 
     if (s0.di != xdi) {
       xdi = s0.di;
-      const GemvDesc& g = desc_at<TABLE>(a, xdi);
+      const auto& g = desc_at<TABLE>(a, xdi);
       const int nul = max(0, min(WB, g.upr - u0));
 #pragma unroll
       for (int w = 0; w < WB; ++w) {
         const bool ok = w < nul;
+        const rsrc_t rx = make_rsrc(g.x, g.x_bytes);
         if constexpr (!BF16) {
-          const uint32_t* x32 = static_cast<const uint32_t*>(g.x) + (u0 + w) * 4;
+          const uint32_t off = ok ? static_cast<uint32_t>(u0 + w) * 16u : kOOB;
           int s = 0;
 #pragma unroll
           for (int d = 0; d < 4; ++d) {
-            xr[w][d] = ok ? x32[d] : 0u;
+            xr[w][d] = ld32(rx, off + 4u * d);
             s = sdot4(xr[w][d], 0x01010101u, s);
           }
           xsum[w] = s;
         } else {
-          const uint16_t* x16 = static_cast<const uint16_t*>(g.x) + (u0 + w) * 16;
+          const uint32_t off = ok ? static_cast<uint32_t>(u0 + w) * 32u : kOOB;
 #pragma unroll
           for (int b = 0; b < 4; ++b)
 #pragma unroll
             for (int h = 0; h < 2; ++h)
-              xr[w][2 * b + h] = ok ? (uint32_t(x16[8 * h + b]) | uint32_t(x16[8 * h + 4 + b]) << 16) : 0u;
+              xr[w][2 * b + h] = uint32_t(ld16(rx, off + 2u * (8 * h + b))) |
+                                 uint32_t(ld16(rx, off + 2u * (8 * h + 4 + b))) << 16;
           xsum[w] = 0;
         }
       }
       load_xscales<NQ>(g, g0, xs);
-      tensor_scale = half_bits_to_float(g.scales[0]);
+      tensor_scale = half_bits_to_float(gp_u16(g.scales)[0]);
       mode = g.mode;
       ydst = g.y;
     }

@@ -18,7 +18,7 @@ inline int bitcos_launch_status() {
 // Resident 256-thread blocks per CU for a kernel.  Queried once per kernel
 // and remembered for the life of the process (a read-mostly cache of a
 // device property, not state that changes results).
-inline int bitcos_blocks_per_cu(const void* fn) {
+inline int bitcos_blocks_per_cu(const void* fn, int threads) {
   static std::mutex mu;
   static std::unordered_map<const void*, int> cache;
   {
@@ -27,21 +27,22 @@ inline int bitcos_blocks_per_cu(const void* fn) {
     if (it != cache.end()) return it->second;
   }
   int nb = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fn, 256, 0) != hipSuccess || nb < 1) nb = 1;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fn, threads, 0) != hipSuccess || nb < 1) nb = 1;
   std::lock_guard<std::mutex> g(mu);
   cache[fn] = nb;
   return nb;
 }
 
-// Blocks for a persistent launch over `units` work units: as many as the GPU
-// keeps resident at once, and no more than one wave (of four per block) per
+// Blocks of `threads` threads for a persistent launch over `units` work units:
+// as many as the GPU keeps resident at once, and no more than one wave per
 // unit.  -1 on a HIP error.
-inline int64_t persistent_blocks(const void* fn, int64_t units) {
+inline int64_t persistent_blocks(const void* fn, int64_t units, int threads = 256) {
   int dev = 0, cus = 0;
   if (hipGetDevice(&dev) != hipSuccess) return -1;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return -1;
-  const int64_t resident = static_cast<int64_t>(cus) * bitcos_blocks_per_cu(fn);
-  const int64_t need = (units + 3) / 4;
+  const int64_t resident = static_cast<int64_t>(cus) * bitcos_blocks_per_cu(fn, threads);
+  const int64_t wpb = threads / 64;
+  const int64_t need = (units + wpb - 1) / wpb;
   int64_t b = need < resident ? need : resident;
   return b < 1 ? 1 : b;
 }
