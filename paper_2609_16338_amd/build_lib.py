@@ -28,7 +28,7 @@ HIP_SOURCES = [
 ]
 HOST_SOURCES = ["host.cpp"]
 
-COMMON = ["-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-function", f"-I{ROOT}/include"]
+COMMON = ["-O3", "-fPIC", "-std=c++20", "-Wall", "-Wno-unused-function", f"-I{ROOT}/include"]
 # Packed fp32 instructions stay off in every device compile.
 DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 

@@ -56,7 +56,8 @@ struct BatchHeader {
   int32_t per_lane;
   int32_t seg;
   int64_t total_units;
-  int32_t reserved[22];
+  int32_t unit_is_step;  // every GEMV's unit is one wave step (BITCOS streaming kernel)
+  int32_t reserved[21];
 };
 static_assert(sizeof(BatchHeader) == 128, "BatchHeader is 128 bytes");
 

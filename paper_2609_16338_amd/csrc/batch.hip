@@ -119,6 +119,7 @@ int bitcos_batch_build(int32_t count, const bitcos_layout* layouts, const void* 
   bitcos::GemvDesc* descs =
       reinterpret_cast<bitcos::GemvDesc*>(static_cast<uint8_t*>(table) + sizeof(bitcos::BatchHeader));
   int64_t units = 0;
+  h.unit_is_step = 1;
   for (int32_t i = 0; i < count; ++i) {
     const bitcos_layout* L = &layouts[i];
     if (L->format != h.format) return BITCOS_E_UNSUPPORTED;
@@ -136,6 +137,7 @@ int bitcos_batch_build(int32_t count, const bitcos_layout* layouts, const void* 
     if (st) return st;
     descs[i].unit_begin = units;
     units += descs[i].units;
+    if (descs[i].unit_rows != rows) h.unit_is_step = 0;
   }
   h.total_units = units;
   memcpy(table, &h, sizeof(h));

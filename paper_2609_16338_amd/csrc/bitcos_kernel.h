@@ -76,7 +76,7 @@ struct KernelArgs {
 //           high byte of -0.5 / +0.5).
 template <bool BF16>
 struct Cfg {
-  static constexpr int kThreads = BF16 ? 256 : 512;  // workgroup size
+  static constexpr int kThreads = BF16 ? 384 : 512;  // workgroup size
   static constexpr int kCopies = BF16 ? 8 : 16;      // table copies
 };
 
@@ -96,41 +96,33 @@ struct Tables<true> {
 template <bool BF16>
 __device__ __forceinline__ void build_tables(Tables<BF16>& t, int tid) {
   constexpr int NC = Cfg<BF16>::kCopies;
-  constexpr int PASSES = 256 * NC / Cfg<BF16>::kThreads;
-  const int e = tid & 255;
-  uint32_t g[8];
+  for (int idx = tid; idx < 256 * NC; idx += Cfg<BF16>::kThreads) {
+    const int e = idx & 255;
+    const int c = idx >> 8;
+    uint32_t g[8];
 #pragma unroll
-  for (int b = 0; b < 8; ++b) g[b] = (e >> b & 1) ? (BF16 ? 0xBF : 0xFF) : (BF16 ? 0x3F : 0x01);
-  const uint2 gv = make_uint2(bytes4(g[0], g[1], g[2], g[3]), bytes4(g[4], g[5], g[6], g[7]));
-  if constexpr (!BF16) {
-    uint32_t sb[8];
-    int q = 0;
+    for (int b = 0; b < 8; ++b) g[b] = (e >> b & 1) ? (BF16 ? 0xBF : 0xFF) : (BF16 ? 0x3F : 0x01);
+    const uint2 gv = make_uint2(bytes4(g[0], g[1], g[2], g[3]), bytes4(g[4], g[5], g[6], g[7]));
+    if constexpr (!BF16) {
+      uint32_t sb[8];
+      int q = 0;
 #pragma unroll
-    for (int b = 0; b < 8; ++b) sb[b] = 0x0C;
+      for (int b = 0; b < 8; ++b) sb[b] = 0x0C;
 #pragma unroll
-    for (int b = 0; b < 8; ++b)
-      if (e >> b & 1) sb[q++] = b;
-    const uint2 sv = make_uint2(bytes4(sb[0], sb[1], sb[2], sb[3]), bytes4(sb[4], sb[5], sb[6], sb[7]));
-#pragma unroll
-    for (int p = 0; p < PASSES; ++p) {
-      const int c = (tid >> 8) + p * (Cfg<BF16>::kThreads / 256);
-      t.sel[e * NC + c] = sv;
+      for (int b = 0; b < 8; ++b)
+        if (e >> b & 1) sb[q++] = b;
+      t.sel[e * NC + c] = make_uint2(bytes4(sb[0], sb[1], sb[2], sb[3]), bytes4(sb[4], sb[5], sb[6], sb[7]));
       t.tsg[e * NC + c] = gv;
-    }
-  } else {
-    uint32_t hi[8];
-    int r = 0;
+    } else {
+      uint32_t hi[8];
+      int r = 0;
 #pragma unroll
-    for (int b = 0; b < 8; ++b) {
-      hi[b] = (e >> b & 1) ? uint32_t(r) : 0x0Cu;
-      r += e >> b & 1;
-    }
-    const uint4 sv = make_uint4(bytes4(0x0C, hi[0], 0x0C, hi[1]), bytes4(0x0C, hi[2], 0x0C, hi[3]),
-                                bytes4(0x0C, hi[4], 0x0C, hi[5]), bytes4(0x0C, hi[6], 0x0C, hi[7]));
-#pragma unroll
-    for (int p = 0; p < PASSES; ++p) {
-      const int c = (tid >> 8) + p * (Cfg<BF16>::kThreads / 256);
-      t.selb[e * NC + c] = sv;
+      for (int b = 0; b < 8; ++b) {
+        hi[b] = (e >> b & 1) ? uint32_t(r) : 0x0Cu;
+        r += e >> b & 1;
+      }
+      t.selb[e * NC + c] = make_uint4(bytes4(0x0C, hi[0], 0x0C, hi[1]), bytes4(0x0C, hi[2], 0x0C, hi[3]),
+                                      bytes4(0x0C, hi[4], 0x0C, hi[5]), bytes4(0x0C, hi[6], 0x0C, hi[7]));
       t.tsh[e * NC + c] = gv;
     }
   }

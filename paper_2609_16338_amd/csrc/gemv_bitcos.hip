@@ -5,6 +5,7 @@
 
 #include "../../include/bitcos.h"
 #include "batch.h"
+#include "bitcos_fast.h"
 #include "bitcos_kernel.h"
 #include "launch_common.h"
 #include "plan.h"
@@ -15,6 +16,11 @@ KernelFn pick_seg_8(int per_lane, bool bf16, bool table);
 KernelFn pick_seg_16(int per_lane, bool bf16, bool table);
 KernelFn pick_seg_32(int per_lane, bool bf16, bool table);
 KernelFn pick_seg_64(int per_lane, bool bf16, bool table);
+FastFn pick_fast_seg_4(int per_lane, bool bf16, bool table);
+FastFn pick_fast_seg_8(int per_lane, bool bf16, bool table);
+FastFn pick_fast_seg_16(int per_lane, bool bf16, bool table);
+FastFn pick_fast_seg_32(int per_lane, bool bf16, bool table);
+FastFn pick_fast_seg_64(int per_lane, bool bf16, bool table);
 }  // namespace bitcos_k
 
 namespace bitcos {
@@ -30,9 +36,22 @@ static bitcos_k::KernelFn pick_bitcos(int per_lane, int seg, bool bf16, bool tab
   }
 }
 
+static bitcos_k::FastFn pick_bitcos_fast(int per_lane, int seg, bool bf16, bool table) {
+  switch (seg) {
+    case 4: return bitcos_k::pick_fast_seg_4(per_lane, bf16, table);
+    case 8: return bitcos_k::pick_fast_seg_8(per_lane, bf16, table);
+    case 16: return bitcos_k::pick_fast_seg_16(per_lane, bf16, table);
+    case 32: return bitcos_k::pick_fast_seg_32(per_lane, bf16, table);
+    case 64: return bitcos_k::pick_fast_seg_64(per_lane, bf16, table);
+    default: return nullptr;
+  }
+}
+
 int launch_bitcos(const BatchHeader& h, const GemvDesc* table_dev, const GemvDesc& one, void* stream) {
   const bool bf16 = h.x_dtype == BITCOS_X_BF16;
-  bitcos_k::KernelFn fn = pick_bitcos(h.per_lane, h.seg, bf16, table_dev != nullptr);
+  // Streaming kernel when every unit is one wave step; the general kernel otherwise.
+  bitcos_k::KernelFn fn = h.unit_is_step ? pick_bitcos_fast(h.per_lane, h.seg, bf16, table_dev != nullptr)
+                                         : pick_bitcos(h.per_lane, h.seg, bf16, table_dev != nullptr);
   if (!fn) return BITCOS_E_UNSUPPORTED;
   bitcos_k::KernelArgs a;
   a.table = table_dev;
@@ -69,5 +88,6 @@ extern "C" int bitcos_gemv(const bitcos_layout* L, const void* blob_dev, int32_t
   st = bitcos::tile_for(L, x_dtype, &h.per_lane, &h.seg, &rows);
   if (st) return st;
   h.total_units = d.units;
+  h.unit_is_step = d.unit_rows == rows;
   return bitcos::launch_bitcos(h, nullptr, d, stream);
 }
