@@ -35,7 +35,8 @@ struct GemvDesc {
   uint32_t signs_bytes;     // bytes of the sign stream (with its zero tail)
   uint32_t scales_bytes;    // bytes of the scales
   uint32_t x_bytes;         // bytes of the activations
-  int32_t reserved[3];
+  uint32_t y_bytes;         // bytes of the output (4 per row)
+  int32_t reserved[2];
 };
 static_assert(sizeof(GemvDesc) == 128, "GemvDesc is 128 bytes");
 

@@ -72,6 +72,7 @@ int make_desc(const bitcos_layout* L, const void* blob_dev, const void* x_dev, c
   d->sec0_bytes = static_cast<uint32_t>(L->sec_bytes[0]);
   d->scales_bytes = static_cast<uint32_t>(L->sec_bytes[BITCOS_SEC_SCALES]);
   d->x_bytes = static_cast<uint32_t>(L->k) * (x_dtype == BITCOS_X_BF16 ? 2u : 1u);
+  d->y_bytes = static_cast<uint32_t>(L->n) * 4u;
   d->mode = (L->group == 128 ? kModeGrouped : 0) | (xscale_dev ? kModeXscale : 0) |
             (y_mode == BITCOS_Y_I32_RAW ? kModeRaw : 0);
   if (L->format == BITCOS_FMT_BITCOS) {

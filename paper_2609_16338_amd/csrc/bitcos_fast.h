@@ -24,7 +24,13 @@ namespace bitcos_k {
 
 template <int W, bool BF16>
 struct FastCfg {
-  static constexpr int kStages = W <= 8 ? 3 : 2;
+  // Prefetch ring depth.  One step ahead with four waves per SIMD measured
+  // faster than two steps ahead with three (the third stage costs the
+  // registers of the fourth wave).
+  static constexpr int kStages = 2;
+  // Next word's lookups in flight during the current word's arithmetic
+  // (costs one word of lookup registers: 16 int8, 24 bf16).
+  static constexpr bool kPipelined = !BF16 && W <= 8;
   // 16-byte chunks per lane of the largest sign block of one step: 64 lanes x
   // W words of 32 weights, all non-zero, plus the two dwords a window may
   // read past its start.
@@ -32,40 +38,48 @@ struct FastCfg {
   static constexpr int kScratchDw = kSignChunks * 256;
 };
 
+// Wave-uniform description of one step (the R rows of one unit).
 struct FastStep {
-  int di;
-  int row0;
-  int nrows;
+  int di;         // descriptor
+  int row0;       // first row
   uint32_t off0;  // first sign bit of the step
-  uint32_t d0;    // first sign dword of the block
+  uint32_t off1;  // first sign bit of the next step
   bool valid;
 };
 
+// Walks a wave's contiguous unit range.  The fields of the current GEMV are
+// read once when the range enters it, not per step.
 template <int R, bool TABLE>
 struct FastGen {
   int di;
-  int64_t U, Uend;
+  int U, Uend;           // the launch's units fit in 31 bits (checked on the host)
+  int begin, end;        // unit range of GEMV di in the launch
+  const uint32_t* offs;  // its unit offsets
+
+  __device__ __forceinline__ void enter(const KernelArgs& a, int d) {
+    di = __builtin_amdgcn_readfirstlane(d);
+    const auto& g = desc_at<TABLE>(a, di);
+    begin = static_cast<int>(g.unit_begin);
+    end = static_cast<int>(g.unit_begin + g.units);
+    offs = g.offsets;
+  }
 
   __device__ __forceinline__ FastStep next(const KernelArgs& a) {
     FastStep s;
     s.valid = U < Uend;
     s.di = di;
     s.row0 = 0;
-    s.nrows = 0;
     s.off0 = 0;
-    s.d0 = 0;
+    s.off1 = 0;
     if (!s.valid) return s;
     if constexpr (TABLE) {
-      while (di + 1 < a.count && U >= desc_at<TABLE>(a, di).unit_begin + desc_at<TABLE>(a, di).units) ++di;
-      di = __builtin_amdgcn_readfirstlane(di);
+      while (U >= end) enter(a, di + 1);  // ends: the last GEMV's end is the total
     }
-    const auto& g = desc_at<TABLE>(a, di);
-    const int u = static_cast<int>(U - g.unit_begin);
+    const int u = U - begin;
     s.di = di;
     s.row0 = u * R;
-    s.nrows = min(R, g.n - s.row0);
-    s.off0 = cp_u32(g.offsets)[u];
-    s.d0 = s.off0 >> 5;
+    s.off0 = cp_u32(offs)[u];
+    s.off1 = cp_u32(offs)[u + 1];
     ++U;
     return s;
   }
@@ -83,18 +97,24 @@ __global__ void __launch_bounds__(Cfg<BF16>::kThreads) bitcos_fast_kernel(const 
   using Ends = GroupEnds<W, 4>;
   constexpr int NQ = Ends::kNQ;
 
-  __shared__ Tables<BF16> tab;
-  __shared__ uint4 scratch[WPB][SCR / 4];
+  // One LDS object: the waves' sign scratch first, then the decode tables.
+  struct Lds {
+    uint4 scratch[WPB * SCR / 4];
+    Tables<BF16> tab;
+  };
+  __shared__ Lds lds;
+  Tables<BF16>& tab = lds.tab;
   build_tables<BF16>(tab, threadIdx.x);
   __syncthreads();
 
   const int lane = threadIdx.x & 63;
   const int wv = threadIdx.x >> 6;
   const int wave = __builtin_amdgcn_readfirstlane(blockIdx.x * WPB + wv);
-  const int64_t nwaves = static_cast<int64_t>(gridDim.x) * WPB;
-  const int64_t per = (a.total_units + nwaves - 1) / nwaves;
-  const int64_t U0 = per * wave;
-  const int64_t U1 = min(U0 + per, a.total_units);
+  const int total = static_cast<int>(a.total_units);
+  const int nwaves = static_cast<int>(gridDim.x) * WPB;
+  const int per = (total + nwaves - 1) / nwaves;
+  const int U0 = per * wave;
+  const int U1 = min(U0 + per, total);
   if (U0 >= U1) return;
 
   const int rho = lane / SEG;
@@ -103,20 +123,25 @@ __global__ void __launch_bounds__(Cfg<BF16>::kThreads) bitcos_fast_kernel(const 
   const int ph = Ends::kAligned ? 0 : (w0 & 3);
   const int g0 = w0 >> 2;
   const int cp = lane & (Cfg<BF16>::kCopies - 1);
-  uint4* scr = scratch[wv];
-  const uint32_t* scr32 = reinterpret_cast<const uint32_t*>(scr);
+  uint4* scr = lds.scratch + wv * (SCR / 4);
+  const uint32_t* scr32 = reinterpret_cast<const uint32_t*>(lds.scratch);
+  // Sign-bit cursors count from the start of the whole scratch array, so a
+  // word's window dword is just cursor / 32.
+  const uint32_t wave_bits = static_cast<uint32_t>(wv) * SCR * 32u;
 
   FastGen<R, TABLE> gen;
-  gen.di = 0;
   gen.U = U0;
   gen.Uend = U1;
-  if constexpr (TABLE) {
-    int lo = 0, hi = a.count;
-    while (hi - lo > 1) {
-      const int mid = (lo + hi) >> 1;
-      if (((CDesc*)a.table)[mid].unit_begin <= U0) lo = mid; else hi = mid;
+  {
+    int lo = 0;
+    if constexpr (TABLE) {  // last descriptor with unit_begin <= U0
+      int hi = a.count;
+      while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (((CDesc*)a.table)[mid].unit_begin <= U0) lo = mid; else hi = mid;
+      }
     }
-    gen.di = __builtin_amdgcn_readfirstlane(lo);
+    gen.enter(a, lo);
   }
 
   // Ring of stages.
@@ -125,43 +150,68 @@ __global__ void __launch_bounds__(Cfg<BF16>::kThreads) bitcos_fast_kernel(const 
   uint4 SV[D][NSC];
   uint16_t SC[D][NQ];
 
+  // Fetch side: buffer resources and lane offsets of the GEMV being fetched.
+  // Per step only the wave-uniform row offset changes (soffset); rows past
+  // the end of a matrix fall outside its resource and read zero.
+  int idi = -1;
+  rsrc_t rb = make_rsrc(nullptr, 0), rg = rb, rs = rb;
+  uint32_t row_bytes = 0, row_scale_bytes = 0;
+  bool grouped = false;
+  uint32_t voff_p = 0;
+  uint32_t voff_q[NQ];
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) voff_q[q] = 0;
+  const uint32_t voff_s = 16u * static_cast<uint32_t>(lane);
+
+  auto fetch_enter = [&](int d) {
+    idi = d;
+    const auto& g = desc_at<TABLE>(a, d);
+    rb = make_rsrc(g.sec0, g.sec0_bytes);
+    rg = make_rsrc(g.signs, g.signs_bytes);
+    rs = make_rsrc(g.scales, g.scales_bytes);
+    row_bytes = static_cast<uint32_t>(g.upr) * 4u * R;
+    row_scale_bytes = static_cast<uint32_t>(g.ngroups) * 2u * R;
+    grouped = (g.mode & kModeGrouped) != 0;
+    voff_p = (__umul24(static_cast<uint32_t>(rho), static_cast<uint32_t>(g.upr)) + static_cast<uint32_t>(w0)) * 4u;
+    const int glast = max(g.ngroups - 1, 0);
+#pragma unroll
+    for (int q = 0; q < NQ; ++q)
+      voff_q[q] = (__umul24(static_cast<uint32_t>(rho), static_cast<uint32_t>(g.ngroups)) +
+                   static_cast<uint32_t>(min(g0 + q, glast))) * 2u;
+  };
+
   auto issue = [&](auto stage_c) {
     constexpr int k = decltype(stage_c)::value;
     const FastStep& s = st[k];
-    const auto& g = desc_at<TABLE>(a, s.di);
-    const int row = s.row0 + rho;
-    const int nwl = max(0, min(W, g.upr - w0));
-    const bool act = s.valid && rho < s.nrows;
-    const rsrc_t rb = make_rsrc(g.sec0, g.sec0_bytes);
-    const uint32_t off = act ? (static_cast<uint32_t>(row) * g.upr + w0) * 4u : kOOB;
+    if (s.valid && s.di != idi) fetch_enter(s.di);
+    const uint32_t unit = static_cast<uint32_t>(s.row0 / R);
+    const uint32_t soff_p = __builtin_amdgcn_readfirstlane(s.valid ? unit * row_bytes : kOOB);
 #pragma unroll
-    for (int w = 0; w < W; ++w) {
-      const uint32_t v = ld32(rb, off + 4u * w);
-      P[k][w] = w < nwl ? v : 0u;
-    }
-    const rsrc_t rg = make_rsrc(g.signs, g.signs_bytes);
-    const uint32_t soff = s.valid ? (s.d0 + 4u * lane) * 4u : kOOB;
+    for (int w = 0; w < W; ++w) P[k][w] = __builtin_amdgcn_raw_buffer_load_b32(rb, voff_p + 4u * w, soff_p, 0);
+    // The step's sign block: dwords [off0 / 32, off1 / 32 + 1] are the most
+    // any window reads; chunks past that are not fetched.
+    const uint32_t d0 = s.off0 >> 5;
+    const uint32_t need = ((s.off1 >> 5) + 2u - d0) * 4u;
 #pragma unroll
     for (int c = 0; c < NSC; ++c) {
-      SV[k][c] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rg, soff + 1024u * c, 0, 0));
+      const uint32_t soff_s = __builtin_amdgcn_readfirstlane((s.valid && 1024u * c < need) ? d0 * 4u + 1024u * c : kOOB);
+      SV[k][c] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rg, voff_s, soff_s, 0));
     }
-    const rsrc_t rs = make_rsrc(g.scales, g.scales_bytes);
-    const bool grouped = (g.mode & kModeGrouped) != 0;
-    const uint32_t qoff = (act && grouped) ? static_cast<uint32_t>(row) * g.ngroups * 2u : kOOB;
+    const uint32_t soff_q = __builtin_amdgcn_readfirstlane((s.valid && grouped) ? unit * row_scale_bytes : kOOB);
 #pragma unroll
-    for (int q = 0; q < NQ; ++q) {
-      const int gi = min(g0 + q, max(g.ngroups - 1, 0));
-      SC[k][q] = ld16(rs, qoff + 2u * gi);
-    }
+    for (int q = 0; q < NQ; ++q) SC[k][q] = __builtin_amdgcn_raw_buffer_load_b16(rs, voff_q[q], soff_q, 0);
   };
 
-  // Lane state of the GEMV being decoded.
+  // Decode side: lane state of the GEMV whose steps are being decoded.
   int xdi = -1;
   uint32_t xr[W][NX];
   float xs[NQ];
   float tensor_scale = 0.0f;
   int mode = 0;
-  void* ydst = nullptr;
+  bool ragged = false;
+  int nwl = W;
+  rsrc_t ry = make_rsrc(nullptr, 0);
+  const uint32_t voff_y = 4u * static_cast<uint32_t>(rho);
 
   auto decode = [&](auto stage_c) {
     constexpr int k = decltype(stage_c)::value;
@@ -169,11 +219,13 @@ __global__ void __launch_bounds__(Cfg<BF16>::kThreads) bitcos_fast_kernel(const 
     if (s.di != xdi) {  // entering another GEMV: its activations and scales
       xdi = s.di;
       const auto& g = desc_at<TABLE>(a, xdi);
-      const int nwl = max(0, min(W, g.upr - w0));
+      nwl = g.upr - w0;
+      ragged = g.upr != SEG * W;
+      const int nx = max(0, min(W, nwl));
       const rsrc_t rx = make_rsrc(g.x, g.x_bytes);
 #pragma unroll
       for (int w = 0; w < W; ++w) {
-        const uint32_t off = w < nwl ? static_cast<uint32_t>(w0 + w) * NX * 4u : kOOB;
+        const uint32_t off = w < nx ? static_cast<uint32_t>(w0 + w) * NX * 4u : kOOB;
 #pragma unroll
         for (int d = 0; d < NX; ++d) xr[w][d] = ld32(rx, off + 4u * d);
       }
@@ -184,42 +236,70 @@ __global__ void __launch_bounds__(Cfg<BF16>::kThreads) bitcos_fast_kernel(const 
         xs[q] = (mode & kModeXscale) ? gp_f32(g.xscale)[gi] : 1.0f;
       }
       tensor_scale = half_bits_to_float(gp_u16(g.scales)[0]);
-      ydst = g.y;
+      ry = make_rsrc(g.y, g.y_bytes);
     }
     // Sign block of the step into this wave's scratch.
 #pragma unroll
     for (int c = 0; c < NSC; ++c) scr[lane + 64 * c] = SV[k][c];
+    // Words past the end of a row (ragged tiles only) count as empty.
+    if (ragged) {
+#pragma unroll
+      for (int w = 0; w < W; ++w)
+        if (w >= nwl) P[k][w] = 0u;
+    }
+    const uint32_t (&Pw)[W] = P[k];
     // Cursor: the step's first sign bit, relative to the block's first dword.
     int pc[W];
     int cnt = 0;
 #pragma unroll
     for (int w = 0; w < W; ++w) {
       pc[w] = cnt;
-      cnt += __builtin_popcount(P[k][w]);
+      cnt += __builtin_popcount(Pw[w]);
     }
     const int incl = wave_incl_scan(cnt);
-    const uint32_t base = (s.off0 & 31u) + static_cast<uint32_t>(incl - cnt);
+    const uint32_t base = wave_bits + (s.off0 & 31u) + static_cast<uint32_t>(incl - cnt);
     __builtin_amdgcn_wave_barrier();
+    // Software pipeline over the lane's words: the table lookups of word w+1
+    // are in flight while word w is multiplied.
     Acc run[W];
     Acc acc = Acc(0);
-#pragma unroll
-    for (int w = 0; w < W; ++w) {
+    auto window = [&](int w) {
       const uint32_t b = base + static_cast<uint32_t>(pc[w]);
-      const uint32_t i = b >> 5;
-      const uint32_t S = __builtin_amdgcn_alignbit(scr32[i + 1], scr32[i], b & 31u);
-      if constexpr (BF16)
-        acc = word_bf16(P[k][w], S, xr[w], acc, tab, cp);
-      else
-        acc = word_i8(P[k][w], S, xr[w], acc, tab, cp);
-      run[w] = acc;
+      return __builtin_amdgcn_alignbit(scr32[(b >> 5) + 1], scr32[b >> 5], b);
+    };
+    if constexpr (FastCfg<W, BF16>::kPipelined) {
+      Look<BF16> L = word_look<BF16>(Pw[0], window(0), tab, cp);
+#pragma unroll
+      for (int w = 0; w < W; ++w) {
+        Look<BF16> Ln;
+        if (w + 1 < W) Ln = word_look<BF16>(Pw[w + 1], window(w + 1), tab, cp);
+        acc = word_math<BF16, Acc>(L, xr[w], acc);
+        run[w] = acc;
+        if (w + 1 < W) L = Ln;
+      }
+    } else if constexpr (W <= 8) {
+#pragma unroll
+      for (int w = 0; w < W; ++w) {
+        acc = word_math<BF16, Acc>(word_look<BF16>(Pw[w], window(w), tab, cp), xr[w], acc);
+        run[w] = acc;
+      }
+    } else {  // wide tiles: byte-at-a-time words keep the register count down
+#pragma unroll
+      for (int w = 0; w < W; ++w) {
+        if constexpr (BF16)
+          acc = word_bf16(Pw[w], window(w), xr[w], acc, tab, cp);
+        else
+          acc = word_i8(Pw[w], window(w), xr[w], acc, tab, cp);
+        run[w] = acc;
+      }
     }
     __builtin_amdgcn_wave_barrier();
 
-    const int row = s.row0 + rho;
-    const bool live = rho < s.nrows;
+    // One lane per row stores; rows past the end are outside ry and dropped.
+    const uint32_t soff_y = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(s.row0) * 4u);
     if (!BF16 && (mode & kModeRaw)) {
       const int tot = seg_sum<SEG>(static_cast<int>(run[W - 1]));
-      if (j == 0 && live) gp_i32_out(ydst)[row] = tot;
+      if (j == SEG - 1) __builtin_amdgcn_raw_buffer_store_b32(static_cast<uint32_t>(tot), ry, voff_y, soff_y, 0);
       return;
     }
     float part;
@@ -242,7 +322,7 @@ __global__ void __launch_bounds__(Cfg<BF16>::kThreads) bitcos_fast_kernel(const 
       }
       part = seg_sum<SEG>(BF16 ? 2.0f * f : f);
     }
-    if (j == 0 && live) gp_f32_out(ydst)[row] = part;
+    if (j == SEG - 1) __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, part), ry, voff_y, soff_y, 0);
   };
 
   // Prologue: steps 0 .. D-2 in flight.

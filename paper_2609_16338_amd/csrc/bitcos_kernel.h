@@ -130,35 +130,98 @@ __device__ __forceinline__ void build_tables(Tables<BF16>& t, int tid) {
 
 // One 32-weight word, int8 activations: P presence word, S the compact signs
 // of P's non-zeros (bit 0 = first non-zero), x[8] the 32 activations; `cp`
-// is this lane's table copy.
+// is this lane's table copy.  The word is split into its table lookups
+// (word_look_*) and its arithmetic (word_math_*) so a caller can keep the
+// next word's lookups in flight while it multiplies the current one.
+struct LookI8 {
+  uint2 sv[4];  // sel[m] per presence byte
+  uint2 tv[4];  // tsg[s] per presence byte
+};
+
+__device__ __forceinline__ LookI8 word_look_i8(uint32_t P, uint32_t S, const Tables<false>& t, int cp) {
+  constexpr int NC = Cfg<false>::kCopies;
+  LookI8 L;
+  uint32_t r = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t m = __builtin_amdgcn_ubfe(P, 8 * i, 8);
+    const uint32_t s = __builtin_amdgcn_ubfe(S, r, 8);
+    if (i < 3) r = __builtin_popcount(m) + r;
+    L.sv[i] = t.sel[m * NC + cp];
+    L.tv[i] = t.tsg[s * NC + cp];
+  }
+  return L;
+}
+
+__device__ __forceinline__ int word_math_i8(const LookI8& L, const uint32_t* x, int acc) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t c0 = __builtin_amdgcn_perm(x[2 * i + 1], x[2 * i], L.sv[i].x);
+    const uint32_t c1 = __builtin_amdgcn_perm(x[2 * i + 1], x[2 * i], L.sv[i].y);
+    acc = sdot4(c0, L.tv[i].x, acc);
+    acc = sdot4(c1, L.tv[i].y, acc);
+  }
+  return acc;
+}
+
+// Byte-at-a-time form (fewest live registers), for the wide tiles.
 __device__ __forceinline__ int word_i8(uint32_t P, uint32_t S, const uint32_t* x, int acc,
                                        const Tables<false>& t, int cp) {
   constexpr int NC = Cfg<false>::kCopies;
   uint32_t r = 0;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const uint32_t m = (P >> (8 * i)) & 0xFFu;
-    const uint32_t s = (S >> r) & 0xFFu;
+    const uint32_t m = __builtin_amdgcn_ubfe(P, 8 * i, 8);
+    const uint32_t s = __builtin_amdgcn_ubfe(S, r, 8);
     const uint2 sv = t.sel[m * NC + cp];
     const uint2 tv = t.tsg[s * NC + cp];
-    const uint32_t c0 = __builtin_amdgcn_perm(x[2 * i + 1], x[2 * i], sv.x);
-    const uint32_t c1 = __builtin_amdgcn_perm(x[2 * i + 1], x[2 * i], sv.y);
-    acc = sdot4(c0, tv.x, acc);
-    acc = sdot4(c1, tv.y, acc);
+    acc = sdot4(__builtin_amdgcn_perm(x[2 * i + 1], x[2 * i], sv.x), tv.x, acc);
+    acc = sdot4(__builtin_amdgcn_perm(x[2 * i + 1], x[2 * i], sv.y), tv.y, acc);
     r += __builtin_popcount(m);
   }
   return acc;
 }
 
 // Same word with bf16 activations (x[16] = 32 bf16): weights as +-0.5 bf16.
+struct LookBf16 {
+  uint4 sb[4];  // selb[m]
+  uint2 th[4];  // tsh[s]
+};
+
+__device__ __forceinline__ LookBf16 word_look_bf16(uint32_t P, uint32_t S, const Tables<true>& t, int cp) {
+  constexpr int NC = Cfg<true>::kCopies;
+  LookBf16 L;
+  uint32_t r = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t m = __builtin_amdgcn_ubfe(P, 8 * i, 8);
+    const uint32_t s = __builtin_amdgcn_ubfe(S, r, 8);
+    if (i < 3) r = __builtin_popcount(m) + r;
+    L.sb[i] = t.selb[m * NC + cp];
+    L.th[i] = t.tsh[s * NC + cp];
+  }
+  return L;
+}
+
+__device__ __forceinline__ float word_math_bf16(const LookBf16& L, const uint32_t* x, float acc) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    acc = bdot2(__builtin_amdgcn_perm(L.th[i].y, L.th[i].x, L.sb[i].x), x[4 * i + 0], acc);
+    acc = bdot2(__builtin_amdgcn_perm(L.th[i].y, L.th[i].x, L.sb[i].y), x[4 * i + 1], acc);
+    acc = bdot2(__builtin_amdgcn_perm(L.th[i].y, L.th[i].x, L.sb[i].z), x[4 * i + 2], acc);
+    acc = bdot2(__builtin_amdgcn_perm(L.th[i].y, L.th[i].x, L.sb[i].w), x[4 * i + 3], acc);
+  }
+  return acc;
+}
+
 __device__ __forceinline__ float word_bf16(uint32_t P, uint32_t S, const uint32_t* x, float acc,
                                            const Tables<true>& t, int cp) {
   constexpr int NC = Cfg<true>::kCopies;
   uint32_t r = 0;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const uint32_t m = (P >> (8 * i)) & 0xFFu;
-    const uint32_t s = (S >> r) & 0xFFu;
+    const uint32_t m = __builtin_amdgcn_ubfe(P, 8 * i, 8);
+    const uint32_t s = __builtin_amdgcn_ubfe(S, r, 8);
     const uint4 sb = t.selb[m * NC + cp];
     const uint2 th = t.tsh[s * NC + cp];
     acc = bdot2(__builtin_amdgcn_perm(th.y, th.x, sb.x), x[4 * i + 0], acc);
@@ -168,6 +231,25 @@ __device__ __forceinline__ float word_bf16(uint32_t P, uint32_t S, const uint32_
     r += __builtin_popcount(m);
   }
   return acc;
+}
+
+template <bool BF16>
+using Look = typename std::conditional<BF16, LookBf16, LookI8>::type;
+
+template <bool BF16>
+__device__ __forceinline__ Look<BF16> word_look(uint32_t P, uint32_t S, const Tables<BF16>& t, int cp) {
+  if constexpr (BF16)
+    return word_look_bf16(P, S, t, cp);
+  else
+    return word_look_i8(P, S, t, cp);
+}
+
+template <bool BF16, class Acc>
+__device__ __forceinline__ Acc word_math(const Look<BF16>& L, const uint32_t* x, Acc acc) {
+  if constexpr (BF16)
+    return word_math_bf16(L, x, acc);
+  else
+    return word_math_i8(L, x, acc);
 }
 
 // The descriptor of GEMV `di` (a wave-uniform index): from the device table
@@ -409,7 +491,7 @@ __global__ void __launch_bounds__(Cfg<BF16>::kThreads) bitcos_gemv_kernel(const 
 
     if (!BF16 && (mode & kModeRaw)) {
       const int tot = seg_sum<SEG>(static_cast<int>(run[W - 1]));
-      if (j == 0 && live) gp_i32_out(ydst)[row] = tot;
+      if (j == SEG - 1 && live) gp_i32_out(ydst)[row] = tot;
       continue;
     }
     float part;
@@ -433,7 +515,7 @@ __global__ void __launch_bounds__(Cfg<BF16>::kThreads) bitcos_gemv_kernel(const 
       }
       part = seg_sum<SEG>(BF16 ? 2.0f * f : f);
     }
-    if (j == 0 && live) gp_f32_out(ydst)[row] = part;
+    if (j == SEG - 1 && live) gp_f32_out(ydst)[row] = part;
   }
 }
 

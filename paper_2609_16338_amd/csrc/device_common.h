@@ -66,19 +66,58 @@ __device__ __forceinline__ int wave_incl_scan(int v) {
 
 __device__ __forceinline__ int lane63(int v) { return __builtin_amdgcn_readlane(v, 63); }
 
-// Sum over aligned segments of SEG lanes (butterfly; every lane of a segment
-// ends with the same value, summed in the same order).
+// Sum over aligned segments of SEG lanes with DPP moves (no LDS traffic).
+// The sum is complete in the segment's last lane (j == SEG - 1); for
+// SEG <= 16 every lane of the segment holds it.  The order of the additions
+// is fixed, so float results are deterministic.
+//   SEG 2, 4: quad_perm swaps (lane ^ 1, lane ^ 2);
+//   SEG 8:    half-row mirror (lane i <-> 7 - i), then the two quad swaps;
+//   SEG 16:   row rotations by 8, 4, 2, 1;
+//   SEG 32:   row sums, then row 1 (3) adds lane 15 of row 0 (2);
+//   SEG 64:   as 32, then row 3 adds lane 31.
+template <int CTRL, int ROWS = 0xF>
+__device__ __forceinline__ int dpp_i(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, ROWS, 0xF, false);
+}
+
 template <int SEG>
 __device__ __forceinline__ int seg_sum(int v) {
-#pragma unroll
-  for (int off = SEG / 2; off >= 1; off /= 2) v += __shfl_xor(v, off, kWave);
+  static_assert(SEG == 2 || SEG == 4 || SEG == 8 || SEG == 16 || SEG == 32 || SEG == 64, "segment");
+  if constexpr (SEG == 8) v += dpp_i<0x141>(v);  // row_half_mirror
+  if constexpr (SEG <= 8) {
+    v += dpp_i<0xB1>(v);                          // quad_perm [1,0,3,2]
+    if constexpr (SEG >= 4) v += dpp_i<0x4E>(v);  // quad_perm [2,3,0,1]
+  } else {
+    v += dpp_i<0x128>(v);  // row_ror:8
+    v += dpp_i<0x124>(v);  // row_ror:4
+    v += dpp_i<0x122>(v);  // row_ror:2
+    v += dpp_i<0x121>(v);  // row_ror:1
+    if constexpr (SEG >= 32) v += dpp_i<0x142, 0xA>(v);  // row_bcast:15 into rows 1, 3
+    if constexpr (SEG == 64) v += dpp_i<0x143, 0x8>(v);  // row_bcast:31 into row 3
+  }
   return v;
+}
+
+template <int CTRL, int ROWS = 0xF>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, ROWS, 0xF, false));
 }
 
 template <int SEG>
 __device__ __forceinline__ float seg_sum(float v) {
-#pragma unroll
-  for (int off = SEG / 2; off >= 1; off /= 2) v += __shfl_xor(v, off, kWave);
+  static_assert(SEG == 2 || SEG == 4 || SEG == 8 || SEG == 16 || SEG == 32 || SEG == 64, "segment");
+  if constexpr (SEG == 8) v += dpp_f<0x141>(v);
+  if constexpr (SEG <= 8) {
+    v += dpp_f<0xB1>(v);
+    if constexpr (SEG >= 4) v += dpp_f<0x4E>(v);
+  } else {
+    v += dpp_f<0x128>(v);
+    v += dpp_f<0x124>(v);
+    v += dpp_f<0x122>(v);
+    v += dpp_f<0x121>(v);
+    if constexpr (SEG >= 32) v += dpp_f<0x142, 0xA>(v);
+    if constexpr (SEG == 64) v += dpp_f<0x143, 0x8>(v);
+  }
   return v;
 }
 

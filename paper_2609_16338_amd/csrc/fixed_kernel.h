@@ -115,7 +115,7 @@ __device__ __forceinline__ void finish_row(int mode, void* ydst, const Acc (&run
   using Ends = GroupEnds<PER, UPG>;
   if (!BF16 && (mode & kModeRaw)) {
     const int tot = seg_sum<SEG>(static_cast<int>(run[PER - 1]));
-    if (j == 0 && live) gp_i32_out(ydst)[row] = tot;
+    if (j == SEG - 1 && live) gp_i32_out(ydst)[row] = tot;
     return;
   }
   float part;
@@ -138,7 +138,7 @@ __device__ __forceinline__ void finish_row(int mode, void* ydst, const Acc (&run
     }
     part = seg_sum<SEG>(f);
   }
-  if (j == 0 && live) gp_f32_out(ydst)[row] = part;
+  if (j == SEG - 1 && live) gp_f32_out(ydst)[row] = part;
 }
 
 // The lane's group scales for one row (grouped mode), else zeros.

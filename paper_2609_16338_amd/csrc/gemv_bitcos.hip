@@ -49,9 +49,11 @@ static bitcos_k::FastFn pick_bitcos_fast(int per_lane, int seg, bool bf16, bool 
 
 int launch_bitcos(const BatchHeader& h, const GemvDesc* table_dev, const GemvDesc& one, void* stream) {
   const bool bf16 = h.x_dtype == BITCOS_X_BF16;
-  // Streaming kernel when every unit is one wave step; the general kernel otherwise.
-  bitcos_k::KernelFn fn = h.unit_is_step ? pick_bitcos_fast(h.per_lane, h.seg, bf16, table_dev != nullptr)
-                                         : pick_bitcos(h.per_lane, h.seg, bf16, table_dev != nullptr);
+  // Streaming kernel when every unit is one wave step (its unit counters are
+  // 32-bit); the general kernel otherwise.
+  const bool streaming = h.unit_is_step && h.total_units < (int64_t(1) << 30);
+  bitcos_k::KernelFn fn = streaming ? pick_bitcos_fast(h.per_lane, h.seg, bf16, table_dev != nullptr)
+                                    : pick_bitcos(h.per_lane, h.seg, bf16, table_dev != nullptr);
   if (!fn) return BITCOS_E_UNSUPPORTED;
   bitcos_k::KernelArgs a;
   a.table = table_dev;
