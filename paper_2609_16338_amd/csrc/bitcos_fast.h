@@ -22,6 +22,11 @@
 
 namespace bitcos_k {
 
+// Workgroup size of the streaming kernel: three waves per SIMD (12 per
+// workgroup, one workgroup per CU, registers capped at 168) where the bf16
+// tile fits, else 512 threads.  Host and device both use it.
+constexpr int fast_threads(int w, bool bf16) { return bf16 && w <= 5 ? 768 : 512; }
+
 template <int W, bool BF16>
 struct FastCfg {
   // Prefetch ring depth.  One step ahead with four waves per SIMD measured
@@ -86,10 +91,10 @@ struct FastGen {
 };
 
 template <int W, int SEG, bool BF16, bool TABLE>
-__global__ void __launch_bounds__(Cfg<BF16>::kThreads) bitcos_fast_kernel(const KernelArgs a) {
+__global__ void __launch_bounds__(fast_threads(W, BF16)) bitcos_fast_kernel(const KernelArgs a) {
   constexpr int R = kWave / SEG;
   constexpr int NX = BF16 ? 16 : 8;
-  constexpr int WPB = Cfg<BF16>::kThreads / kWave;
+  constexpr int WPB = fast_threads(W, BF16) / kWave;
   constexpr int D = FastCfg<W, BF16>::kStages;
   constexpr int NSC = FastCfg<W, BF16>::kSignChunks;
   constexpr int SCR = FastCfg<W, BF16>::kScratchDw;
@@ -104,7 +109,7 @@ __global__ void __launch_bounds__(Cfg<BF16>::kThreads) bitcos_fast_kernel(const 
   };
   __shared__ Lds lds;
   Tables<BF16>& tab = lds.tab;
-  build_tables<BF16>(tab, threadIdx.x);
+  build_tables<BF16>(tab, threadIdx.x, fast_threads(W, BF16));
   __syncthreads();
 
   const int lane = threadIdx.x & 63;
@@ -263,6 +268,7 @@ __global__ void __launch_bounds__(Cfg<BF16>::kThreads) bitcos_fast_kernel(const 
     // are in flight while word w is multiplied.
     Acc run[W];
     Acc acc = Acc(0);
+    // A word's 64-bit window of the sign block, aligned to its first sign.
     auto window = [&](int w) {
       const uint32_t b = base + static_cast<uint32_t>(pc[w]);
       return __builtin_amdgcn_alignbit(scr32[(b >> 5) + 1], scr32[b >> 5], b);
@@ -278,9 +284,14 @@ __global__ void __launch_bounds__(Cfg<BF16>::kThreads) bitcos_fast_kernel(const 
         if (w + 1 < W) L = Ln;
       }
     } else if constexpr (W <= 8) {
+      // Every word's window is read before the first word is decoded, so a
+      // word waits on one LDS round trip (its lookups), not two.
+      uint32_t S[W];
+#pragma unroll
+      for (int w = 0; w < W; ++w) S[w] = window(w);
 #pragma unroll
       for (int w = 0; w < W; ++w) {
-        acc = word_math<BF16, Acc>(word_look<BF16>(Pw[w], window(w), tab, cp), xr[w], acc);
+        acc = word_math<BF16, Acc>(word_look<BF16>(Pw[w], S[w], tab, cp), xr[w], acc);
         run[w] = acc;
       }
     } else {  // wide tiles: byte-at-a-time words keep the register count down

@@ -76,8 +76,8 @@ struct KernelArgs {
 //           high byte of -0.5 / +0.5).
 template <bool BF16>
 struct Cfg {
-  static constexpr int kThreads = BF16 ? 384 : 512;  // workgroup size
-  static constexpr int kCopies = BF16 ? 8 : 16;      // table copies
+  static constexpr int kThreads = 512;  // workgroup size of the general kernel
+  static constexpr int kCopies = 16;    // table copies
 };
 
 template <bool BF16>
@@ -94,9 +94,9 @@ struct Tables<true> {
 };
 
 template <bool BF16>
-__device__ __forceinline__ void build_tables(Tables<BF16>& t, int tid) {
+__device__ __forceinline__ void build_tables(Tables<BF16>& t, int tid, int nthreads) {
   constexpr int NC = Cfg<BF16>::kCopies;
-  for (int idx = tid; idx < 256 * NC; idx += Cfg<BF16>::kThreads) {
+  for (int idx = tid; idx < 256 * NC; idx += nthreads) {
     const int e = idx & 255;
     const int c = idx >> 8;
     uint32_t g[8];
@@ -324,7 +324,7 @@ struct StepGen {
 template <int W, int SEG, bool BF16, bool TABLE>
 __global__ void __launch_bounds__(Cfg<BF16>::kThreads) bitcos_gemv_kernel(const KernelArgs a) {
   __shared__ Tables<BF16> tab;
-  build_tables<BF16>(tab, threadIdx.x);
+  build_tables<BF16>(tab, threadIdx.x, Cfg<BF16>::kThreads);
   __syncthreads();
 
   constexpr int R = kWave / SEG;

@@ -61,7 +61,8 @@ int launch_bitcos(const BatchHeader& h, const GemvDesc* table_dev, const GemvDes
   a.count = h.count;
   a.pad = 0;
   a.one = one;
-  const int threads = bf16 ? bitcos_k::Cfg<true>::kThreads : bitcos_k::Cfg<false>::kThreads;
+  const int threads = streaming ? bitcos_k::fast_threads(h.per_lane, bf16)
+                                : (bf16 ? bitcos_k::Cfg<true>::kThreads : bitcos_k::Cfg<false>::kThreads);
   const int64_t blocks = persistent_blocks(reinterpret_cast<const void*>(fn), h.total_units, threads);
   if (blocks <= 0 || blocks > 0x7FFFFFFF) return BITCOS_E_HIP;
   hipLaunchKernelGGL(fn, dim3(static_cast<unsigned>(blocks)), dim3(threads), 0,
