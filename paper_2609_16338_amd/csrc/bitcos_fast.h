@@ -22,16 +22,19 @@
 
 namespace bitcos_k {
 
-// Workgroup size of the streaming kernel: three waves per SIMD (12 per
-// workgroup, one workgroup per CU, registers capped at 168) where the bf16
-// tile fits, else 512 threads.  Host and device both use it.
-constexpr int fast_threads(int w, bool bf16) { return bf16 && w <= 5 ? 768 : 512; }
+// Workgroup size of the streaming kernel: one workgroup per CU holding as
+// many waves per SIMD as the tile's registers allow (4: <= 128 VGPRs,
+// 3: <= 168, 2: <= 256; the bounds follow the register counts of each
+// instantiation so none spills).  Host and device both use it.
+constexpr int fast_waves_per_simd(int w, bool bf16) {
+  return bf16 ? (w <= 3 ? 4 : w <= 5 ? 3 : 2) : (w <= 5 ? 4 : w <= 8 ? 3 : 2);
+}
+constexpr int fast_threads(int w, bool bf16) { return 256 * fast_waves_per_simd(w, bf16); }
 
 template <int W, bool BF16>
 struct FastCfg {
-  // Prefetch ring depth.  One step ahead with four waves per SIMD measured
-  // faster than two steps ahead with three (the third stage costs the
-  // registers of the fourth wave).
+  // Prefetch ring depth: one step ahead.  Two steps ahead (which fits the
+  // int8 tiles up to five words per lane) measured no faster.
   static constexpr int kStages = 2;
   // Next word's lookups in flight during the current word's arithmetic
   // (costs one word of lookup registers: 16 int8, 24 bf16).
@@ -102,18 +105,19 @@ __global__ void __launch_bounds__(fast_threads(W, BF16)) bitcos_fast_kernel(cons
   using Ends = GroupEnds<W, 4>;
   constexpr int NQ = Ends::kNQ;
 
-  // One LDS object: the waves' sign scratch first, then the decode tables.
-  struct Lds {
-    uint4 scratch[WPB * SCR / 4];
-    Tables<BF16> tab;
-  };
-  __shared__ Lds lds;
-  Tables<BF16>& tab = lds.tab;
+  // Decode tables, and one sign-block buffer per ring stage (each wave owns
+  // SCR dwords of every buffer).  The stage buffers are separate objects so
+  // the compiler can tell that a read of one does not wait on the fetch into
+  // another.
+  __shared__ Tables<BF16> tab;
+  __shared__ uint4 sbuf0[WPB * SCR / 4];
+  __shared__ uint4 sbuf1[WPB * SCR / 4];
+  __shared__ uint4 sbuf2[D > 2 ? WPB * SCR / 4 : 1];
   build_tables<BF16>(tab, threadIdx.x, fast_threads(W, BF16));
   __syncthreads();
 
   const int lane = threadIdx.x & 63;
-  const int wv = threadIdx.x >> 6;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wave = __builtin_amdgcn_readfirstlane(blockIdx.x * WPB + wv);
   const int total = static_cast<int>(a.total_units);
   const int nwaves = static_cast<int>(gridDim.x) * WPB;
@@ -128,10 +132,14 @@ __global__ void __launch_bounds__(fast_threads(W, BF16)) bitcos_fast_kernel(cons
   const int ph = Ends::kAligned ? 0 : (w0 & 3);
   const int g0 = w0 >> 2;
   const int cp = lane & (Cfg<BF16>::kCopies - 1);
-  uint4* scr = lds.scratch + wv * (SCR / 4);
-  const uint32_t* scr32 = reinterpret_cast<const uint32_t*>(lds.scratch);
-  // Sign-bit cursors count from the start of the whole scratch array, so a
-  // word's window dword is just cursor / 32.
+  auto stage_buf = [&](auto stage_c) -> uint4* {
+    constexpr int k = decltype(stage_c)::value;
+    if constexpr (k == 0) return sbuf0;
+    else if constexpr (k == 1) return sbuf1;
+    else return sbuf2;
+  };
+  // Sign-bit cursors count from the start of a stage buffer, so a word's
+  // window dword is just cursor / 32.
   const uint32_t wave_bits = static_cast<uint32_t>(wv) * SCR * 32u;
 
   FastGen<R, TABLE> gen;
@@ -152,7 +160,6 @@ __global__ void __launch_bounds__(fast_threads(W, BF16)) bitcos_fast_kernel(cons
   // Ring of stages.
   FastStep st[D];
   uint32_t P[D][W];
-  uint4 SV[D][NSC];
   uint16_t SC[D][NQ];
 
   // Fetch side: buffer resources and lane offsets of the GEMV being fetched.
@@ -197,10 +204,15 @@ __global__ void __launch_bounds__(fast_threads(W, BF16)) bitcos_fast_kernel(cons
     // any window reads; chunks past that are not fetched.
     const uint32_t d0 = s.off0 >> 5;
     const uint32_t need = ((s.off1 >> 5) + 2u - d0) * 4u;
+    // Straight into this wave's part of the stage buffer: lane l's 16 bytes
+    // of chunk c land at byte 1024 c + 16 l.  Chunks past the step's range
+    // read zero.
+    uint4* dst = stage_buf(stage_c) + wv * (SCR / 4);
 #pragma unroll
     for (int c = 0; c < NSC; ++c) {
       const uint32_t soff_s = __builtin_amdgcn_readfirstlane((s.valid && 1024u * c < need) ? d0 * 4u + 1024u * c : kOOB);
-      SV[k][c] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rg, voff_s, soff_s, 0));
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rg, (__attribute__((address_space(3))) void*)(dst + 64 * c), 16, voff_s,
+                                               soff_s, 0, 0);
     }
     const uint32_t soff_q = __builtin_amdgcn_readfirstlane((s.valid && grouped) ? unit * row_scale_bytes : kOOB);
 #pragma unroll
@@ -243,9 +255,7 @@ __global__ void __launch_bounds__(fast_threads(W, BF16)) bitcos_fast_kernel(cons
       tensor_scale = half_bits_to_float(gp_u16(g.scales)[0]);
       ry = make_rsrc(g.y, g.y_bytes);
     }
-    // Sign block of the step into this wave's scratch.
-#pragma unroll
-    for (int c = 0; c < NSC; ++c) scr[lane + 64 * c] = SV[k][c];
+    const uint32_t* scr32 = reinterpret_cast<const uint32_t*>(stage_buf(stage_c));
     // Words past the end of a row (ragged tiles only) count as empty.
     if (ragged) {
 #pragma unroll
