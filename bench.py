@@ -51,6 +51,12 @@ def parse():
     ap.add_argument("--threads", type=int, default=min(16, os.cpu_count() or 1))
     ap.add_argument("--profile-pass", action="store_true",
                     help="for counter runs: the dominant BITCOS launch x5, then a plain 256 MiB device copy x5")
+    ap.add_argument("--sweep", action="store_true",
+                    help="zero-density sweep on one 8192 x 8192 matrix: BITCOS vs five-trit vs 2-bit (own JSON line)")
+    ap.add_argument("--gamma", action="store_true",
+                    help="two-term roofline: cycles per 32 weights on cache-resident data vs z (own JSON line)")
+    ap.add_argument("--sweep-copies", type=int, default=40,
+                    help="device copies of each swept matrix streamed per launch (> 2 x the 256 MB Infinity Cache)")
     return ap.parse_args()
 
 
@@ -265,10 +271,146 @@ def profile_pass(args):
           flush=True)
 
 
+def sweep(args):
+    """Zero-density sweep: one 8192 x 8192 matrix with group-128 scales per z,
+    batch 1, BITCOS against the five-trit and 2-bit kernels on this GPU.  Each
+    format's blob is copied `--sweep-copies` times in HBM and one persistent
+    launch covers all copies, so every launch streams more than twice the
+    Infinity Cache; time per GEMV = launch time / copies."""
+    import torch
+
+    from paper_2609_16338_amd import _native as N
+    from paper_2609_16338_amd import api
+
+    cid, k = 4, 8192
+    xi = torch.from_numpy(wl.activation_inputs(cid, "int8", 1, k)).cuda().reshape(-1)
+    xb = torch.from_numpy(wl.activation_inputs(cid, "bf16", 1, k).view(np.int16)).view(torch.bfloat16).cuda().reshape(-1)
+    names = {N.FMT_BITCOS: "bitcos", N.FMT_TRIT5: "trit5", N.FMT_BIT2: "bit2"}
+    rows = []
+    for zi, z in enumerate(wl.SWEEP_Z + (0.95,)):  # the paper's extreme point beside the config's five
+        spec = wl.sweep_spec(z)
+        w, sc = wl.matrix_inputs(cid, 0, zi, spec)
+        row = {"z": z, "z_measured": round(float((w == 0).mean()), 5)}
+        for fmt, nm in names.items():
+            L, blob = api.plan_and_pack(fmt, w, sc, spec.group)
+            src = torch.from_numpy(blob).cuda()
+            blobs = [src.clone() for _ in range(args.sweep_copies)]
+            row[f"{nm}_payload_bytes"] = L.payload_bits // 8
+            row[f"{nm}_bpw"] = round(L.payload_bits / (spec.n * spec.k), 5)
+            for kind, x in (("int8", xi), ("bf16", xb)):
+                ys = [torch.empty(spec.n, dtype=torch.float32, device="cuda") for _ in blobs]
+                b = api.Batch([L] * len(blobs), blobs, [x] * len(blobs), ys)
+                g = capture(b.run)
+                ms, _ = time_graph(g, args.steps, args.warmup)
+                us = ms * 1e3 / len(blobs)
+                row[f"{nm}_{kind}_us"] = round(us, 4)
+                row[f"{nm}_{kind}_GBs"] = round(L.payload_bits / 8 / (us * 1e-6) / 1e9, 1)
+                # CU-cycles per 32 weights with the weights streamed from HBM
+                row[f"{nm}_{kind}_gamma_hbm"] = round(32 * CU_COUNT * CLOCK_HZ * us * 1e-6 / (spec.n * spec.k), 3)
+                del g, b, ys
+            del blobs, src
+            torch.cuda.empty_cache()
+        for kind in ("int8", "bf16"):
+            t = row[f"bitcos_{kind}_us"]
+            row[f"speedup_vs_trit5_{kind}"] = round(row[f"trit5_{kind}_us"] / t, 4)
+            row[f"speedup_vs_bit2_{kind}"] = round(row[f"bit2_{kind}_us"] / t, 4)
+        rows.append(row)
+        print(f"[sweep] z={z}: " + ", ".join(f"{nm} {row[f'{nm}_int8_us']:.2f}/{row[f'{nm}_bf16_us']:.2f} us"
+                                            for nm in names.values()), file=sys.stderr, flush=True)
+
+    def crossover(kind):
+        # z where the BITCOS / five-trit time ratio crosses 1 (linear between points)
+        pts = [(r["z"], r[f"speedup_vs_trit5_{kind}"]) for r in rows]
+        for (z0, s0), (z1, s1) in zip(pts, pts[1:]):
+            if (s0 - 1) * (s1 - 1) <= 0 and s1 != s0:
+                return round(z0 + (1 - s0) * (z1 - z0) / (s1 - s0), 4)
+        return None
+
+    print(json.dumps({
+        "metric": "zero-density sweep, 8192x8192 g128, batch 1: per-GEMV time, effective GB/s, speedups",
+        "unit": "us",
+        "copies_per_launch": args.sweep_copies,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "data": "synthetic",
+        "crossover_z_vs_trit5_int8": crossover("int8"),
+        "crossover_z_vs_trit5_bf16": crossover("bf16"),
+        "points": rows,
+    }))
+
+
+GAMMA_Z = (0.30, 0.42, 0.515, 0.95)
+CU_COUNT = 256
+CLOCK_HZ = 2.4e9
+
+
+def gamma(args):
+    """The paper's two-term roofline (Sec. III-B, Eqs. (5)-(6)) on this GPU.
+
+    gamma = CU-cycles one CU spends per 32 weights when the operands are
+    L2-resident (one launch over 64 GEMVs that all read the same 2048 x 8192
+    g128 blob, 3.6-4.4 MB, which each XCD's 4 MB L2 holds, so the instruction
+    stream is the limit and the kernel's prologue is amortised); beta = HBM
+    bytes per CU-cycle at the
+    8 TB/s peak; B(z) = bytes per 32 weights of each layout.  Predicted
+    effective bandwidth = min(beta, B / gamma) per CU, times all CUs."""
+    import torch
+
+    from paper_2609_16338_amd import _native as N
+    from paper_2609_16338_amd import api
+
+    cid, n, k = 6, 2048, 8192
+    beta = HBM_PEAK_GBS * 1e9 / (CU_COUNT * CLOCK_HZ)
+    xi = torch.from_numpy(wl.activation_inputs(cid, "int8", 1, k)).cuda().reshape(-1)
+    xb = torch.from_numpy(wl.activation_inputs(cid, "bf16", 1, k).view(np.int16)).view(torch.bfloat16).cuda().reshape(-1)
+    names = {N.FMT_BITCOS: "bitcos", N.FMT_TRIT5: "trit5", N.FMT_BIT2: "bit2"}
+    rows = []
+    for zi, z in enumerate(GAMMA_Z):
+        spec = wl.MatrixSpec(f"gamma_z{z}", n, k, z, 128, 0.01, 0.1)
+        w, sc = wl.matrix_inputs(cid, 0, zi, spec)
+        row = {"z": z, "z_measured": round(float((w == 0).mean()), 5)}
+        for fmt, nm in names.items():
+            L, blob = api.plan_and_pack(fmt, w, sc, spec.group)
+            dev = torch.from_numpy(blob).cuda()
+            b32 = L.payload_bits / 8 / (n * k) * 32
+            row[f"{nm}_bytes_per_32"] = round(b32, 4)
+            reps = 64
+            devs = [dev] * reps
+            for kind, x in (("int8", xi), ("bf16", xb)):
+                ys = [torch.empty(n, dtype=torch.float32, device="cuda") for _ in range(reps)]
+                b = api.Batch([L] * reps, devs, [x] * reps, ys)
+                g = capture(b.run)
+                ms, _ = time_graph(g, max(args.steps, 50), args.warmup)
+                rate = reps * n * k / (ms * 1e-3)
+                gam = 32 * CU_COUNT * CLOCK_HZ / rate
+                row[f"{nm}_{kind}_gamma"] = round(gam, 3)
+                row[f"{nm}_{kind}_pred_GBs"] = round(min(beta, b32 / gam) * CU_COUNT * CLOCK_HZ / 1e9, 1)
+                row[f"{nm}_{kind}_bound"] = "memory" if b32 / gam > beta else "instructions"
+                del g, b, ys
+            del devs
+        rows.append(row)
+        print(f"[gamma] z={z}: " + ", ".join(f"{nm} {row[f'{nm}_int8_gamma']:.2f}/{row[f'{nm}_bf16_gamma']:.2f}"
+                                            for nm in names.values()), file=sys.stderr, flush=True)
+    print(json.dumps({
+        "metric": "two-term roofline: gamma = CU-cycles per 32 weights, L2-resident 2048x8192 g128 (x64 per launch), batch 1",
+        "beta_bytes_per_cu_cycle": round(beta, 4),
+        "clock_hz": CLOCK_HZ,
+        "cus": CU_COUNT,
+        "data": "synthetic",
+        "points": rows,
+    }))
+
+
 def main():
     args = parse()
+    if args.gamma:
+        gamma(args)
+        return
     if args.profile_pass:
         profile_pass(args)
+        return
+    if args.sweep:
+        sweep(args)
         return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
