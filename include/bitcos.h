@@ -216,6 +216,35 @@ int bitcos_gemv_batch(const void* table_host, const void* table_dev, void* strea
 int bitcos_quantize_act(const void* x_bf16_dev, int32_t m, int32_t k, int8_t* q_dev,
                         float* scale_dev, void* stream);
 
+/* ---- device-side BITCOS packer ------------------------------------------
+ * The same blob bytes as bitcos_plan + bitcos_pack (Sec. II-A: presence
+ * bitmap and compacted sign vector in row-major order, the unit offsets and
+ * the scales), computed on the GPU from W already in device memory.  Both
+ * calls enqueue on `stream` and wait for it before returning (the plan has
+ * to read the non-zero count back).
+ *
+ * bitcos_plan_device_workspace: bytes of device workspace for an n-row
+ *   matrix (0 if n < 1): a 16-byte header and n + 1 row offsets.
+ *
+ * bitcos_plan_device: W is device int8 [n][k], row-major; group / unit_rows
+ *   as bitcos_plan (n*k < 2^31).  ws_dev: caller device memory of ws_bytes
+ *   >= bitcos_plan_device_workspace(n); it receives the row offsets the pack
+ *   call reuses.  Fills *out exactly as bitcos_plan would.  Errors: E_ARG,
+ *   E_SPACE (workspace), E_VALUE (a weight outside {-1,0,1}), E_UNSUPPORTED
+ *   (shape), E_HIP.
+ *
+ * bitcos_pack_device: writes the blob into dst_dev (device, cap >=
+ *   L->total_bytes) from the same W, the device fp16 scales ([n][k/128] or
+ *   [1], finite and non-negative) and the workspace of the plan call for this
+ *   W and *L.  Errors: E_ARG (a layout this plan would not give), E_SPACE,
+ *   E_VALUE (bad scale, or W differs from the planned one: then the blob is
+ *   incomplete but nothing outside it is written), E_UNSUPPORTED, E_HIP. */
+size_t bitcos_plan_device_workspace(int32_t n);
+int bitcos_plan_device(const int8_t* w_dev, int32_t n, int32_t k, int32_t group, int32_t unit_rows,
+                       void* ws_dev, size_t ws_bytes, bitcos_layout* out, void* stream);
+int bitcos_pack_device(const int8_t* w_dev, const uint16_t* scales_dev, const bitcos_layout* L,
+                       void* ws_dev, size_t ws_bytes, void* dst_dev, size_t cap, void* stream);
+
 /* ---- launch description (for measurement) ---------------------------------
  * Fills the kernel configuration a GEMV on this layout would launch with:
  * words (or blocks) per lane, lanes per row segment, rows per wave step,

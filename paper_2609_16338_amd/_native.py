@@ -93,6 +93,9 @@ SIGNATURES = {
     "bitcos_batch_bytes": (ctypes.c_size_t, [_I32]),
     "bitcos_batch_build": (ctypes.c_int, [_I32, _P, _P, _P, _P, _P, _I32, _I32, _P, _SZ]),
     "bitcos_gemv_batch": (ctypes.c_int, [_P, _P, _P]),
+    "bitcos_plan_device_workspace": (ctypes.c_size_t, [_I32]),
+    "bitcos_plan_device": (ctypes.c_int, [_P, _I32, _I32, _I32, _I32, _P, _SZ, _LP, _P]),
+    "bitcos_pack_device": (ctypes.c_int, [_P, _P, _LP, _P, _SZ, _P, _SZ, _P]),
 }
 
 

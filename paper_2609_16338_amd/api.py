@@ -120,6 +120,32 @@ def plan_and_pack(fmt: int, w, scales, group: int = 128, unit_rows: int = 0):
     raise ValueError(f"unknown format {fmt}")
 
 
+def bitcos_pack_device(w_dev, scales_dev, group: int = 128, unit_rows: int = 0, stream=None):
+    """(layout, device blob) packed on the GPU from device tensors: W int8 [n][k]
+    and fp16 scales ([n][k/128] or [1]).  Same bytes as the host packer."""
+    import torch
+    if w_dev.dtype != torch.int8 or w_dev.dim() != 2 or not w_dev.is_cuda or not w_dev.is_contiguous():
+        raise ValueError("w_dev must be a contiguous 2-D int8 CUDA tensor")
+    if scales_dev.dtype not in (torch.float16, torch.int16) or not scales_dev.is_cuda or not scales_dev.is_contiguous():
+        raise ValueError("scales_dev must be a contiguous fp16 CUDA tensor")
+    n, k = w_dev.shape
+    ws_bytes = N.lib().bitcos_plan_device_workspace(n)
+    ws = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device=w_dev.device)
+    L = Layout()
+    h = _stream_handle(stream)
+    N.check(N.lib().bitcos_plan_device(ctypes.c_void_p(w_dev.data_ptr()), n, k, group, unit_rows,
+                                       ctypes.c_void_p(ws.data_ptr()), ws_bytes, ctypes.byref(L), h),
+            "bitcos_plan_device")
+    if scales_dev.numel() != num_scales(L):
+        raise ValueError(f"scales_dev has {scales_dev.numel()} values, layout needs {num_scales(L)}")
+    blob = torch.empty(L.total_bytes, dtype=torch.uint8, device=w_dev.device)
+    N.check(N.lib().bitcos_pack_device(ctypes.c_void_p(w_dev.data_ptr()), ctypes.c_void_p(scales_dev.data_ptr()),
+                                       ctypes.byref(L), ctypes.c_void_p(ws.data_ptr()), ws_bytes,
+                                       ctypes.c_void_p(blob.data_ptr()), L.total_bytes, h),
+            "bitcos_pack_device")
+    return L, blob
+
+
 # ---------------------------------------------------------------------------
 # GEMV (device)
 # ---------------------------------------------------------------------------

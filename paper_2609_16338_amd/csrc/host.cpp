@@ -98,19 +98,16 @@ const char* bitcos_strerror(int status) {
 
 uint32_t bitcos_version(void) { return BITCOS_LAYOUT_VERSION; }
 
+}  // extern "C"
+
 // ---------------------------------------------------------------------------
 // BITCOS
 // ---------------------------------------------------------------------------
 
-int bitcos_plan(const int8_t* w, int32_t n, int32_t k, int32_t group, int32_t unit_rows,
-                bitcos_layout* out) {
-  if (!out) return BITCOS_E_ARG;
-  int st = check_common(w, n, k, group, group == 128 ? 128 : 32);
-  if (st) return st;
-  if (unit_rows < 0) return BITCOS_E_ARG;
-  uint64_t nnz = 0;
-  st = count_nnz(w, int64_t(n) * k, &nnz);
-  if (st) return st;
+namespace bitcos {
+
+int bitcos_layout_for(int32_t n, int32_t k, int32_t group, int32_t unit_rows, uint64_t nnz,
+                      bitcos_layout* out) {
   if (nnz > 0xFFFFFFFFull) return BITCOS_E_UNSUPPORTED;  // 32-bit sign offsets
   if (unit_rows == 0) unit_rows = bitcos::bitcos_default_unit_rows(n, k);
   bitcos_layout L;
@@ -134,6 +131,22 @@ int bitcos_plan(const int8_t* w, int32_t n, int32_t k, int32_t group, int32_t un
   L.payload_bits = uint64_t(n) * uint64_t(k) + nnz + 16ull * uint64_t(ns);
   *out = L;
   return BITCOS_OK;
+}
+
+}  // namespace bitcos
+
+extern "C" {
+
+int bitcos_plan(const int8_t* w, int32_t n, int32_t k, int32_t group, int32_t unit_rows,
+                bitcos_layout* out) {
+  if (!out) return BITCOS_E_ARG;
+  int st = check_common(w, n, k, group, group == 128 ? 128 : 32);
+  if (st) return st;
+  if (unit_rows < 0) return BITCOS_E_ARG;
+  uint64_t nnz = 0;
+  st = count_nnz(w, int64_t(n) * k, &nnz);
+  if (st) return st;
+  return bitcos::bitcos_layout_for(n, k, group, unit_rows, nnz, out);
 }
 
 int bitcos_pack(const int8_t* w, const uint16_t* scales_f16, const bitcos_layout* L, void* dst,

@@ -65,4 +65,11 @@ inline int bitcos_default_unit_rows(int n, int k) {
   return t.rows;
 }
 
+// BITCOS layout (section placement, sizes, payload bits) of an n x k matrix
+// with `nnz` non-zeros; unit_rows 0 = the default.  Shared by the host and
+// device packers so both place every section identically.  Defined in
+// host.cpp.
+int bitcos_layout_for(int32_t n, int32_t k, int32_t group, int32_t unit_rows, uint64_t nnz,
+                      struct bitcos_layout* out);
+
 }  // namespace bitcos
