@@ -502,7 +502,7 @@ def main():
         "speedup_vs_bit2": round(res[(N.FMT_BIT2, "int8")] / ms8, 4) if N.FMT_TRIT5 in fmts else None,
     }
     info = api.describe(top.entries[0][3], 1, N.X_BF16)
-    streaming = all(e[3].unit_rows == info.rows_per_step for e in top.entries)
+    streaming = all(info.rows_per_step % e[3].unit_rows == 0 for e in top.entries)
     kname = "bitcos_fast_kernel" if streaming else "bitcos_gemv_kernel"
     out["roofline"] = {
         "bound": "hbm",

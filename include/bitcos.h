@@ -118,7 +118,7 @@ uint32_t bitcos_version(void);
  * bitcos_plan: validate W (host int8 [n][k], row-major, values in {-1,0,1})
  * and fill *out.  group is 128 (k % 128 == 0) or 0 (one scale per tensor,
  * k % 32 == 0).  unit_rows >= 1 sets the rows per sign offset; 0 picks the
- * library default for (n, k) (the GEMV's rows per wave).  Errors: E_ARG,
+ * library default (1: one offset per row, which every kernel can use).  Errors: E_ARG,
  * E_VALUE (a weight outside {-1,0,1}).  Paper: Sec. II-A. */
 int bitcos_plan(const int8_t* w, int32_t n, int32_t k, int32_t group, int32_t unit_rows,
                 bitcos_layout* out);

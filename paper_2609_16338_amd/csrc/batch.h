@@ -36,7 +36,8 @@ struct GemvDesc {
   uint32_t scales_bytes;    // bytes of the scales
   uint32_t x_bytes;         // bytes of the activations
   uint32_t y_bytes;         // bytes of the output (4 per row)
-  int32_t reserved[2];
+  int32_t offset_stride;    // streaming kernel: offset entries per wave step (its unit), else 0
+  int32_t offset_last;      // index of the last offset entry (= nnz)
 };
 static_assert(sizeof(GemvDesc) == 128, "GemvDesc is 128 bytes");
 
@@ -74,6 +75,10 @@ int launch_fixed(const BatchHeader& h, const GemvDesc* table_dev, const GemvDesc
 
 // Tile (per-lane units, lanes per row) the given layout runs with.
 int tile_for(const bitcos_layout* L, int32_t x_dtype, int* per_lane, int* seg, int* rows);
+
+// Count the descriptor's units in wave steps of `rows` rows for the
+// streaming BITCOS kernel; possible when the layout's unit divides the step.
+bool to_step_units(GemvDesc* d, int rows);
 
 // Fill one descriptor from a layout and device pointers (unit_begin = 0).
 int make_desc(const bitcos_layout* L, const void* blob_dev, const void* x_dev, const float* xscale_dev,

@@ -88,7 +88,16 @@ int make_desc(const bitcos_layout* L, const void* blob_dev, const void* x_dev, c
   }
   d->unit_begin = 0;
   d->units = (L->n + d->unit_rows - 1) / d->unit_rows;
+  d->offset_last = static_cast<int32_t>(d->units);
+  d->offset_stride = 0;
   return BITCOS_OK;
+}
+
+bool to_step_units(GemvDesc* d, int rows) {
+  if (d->unit_rows < 1 || rows % d->unit_rows) return false;
+  d->offset_stride = rows / d->unit_rows;
+  d->units = (d->n + rows - 1) / rows;
+  return true;
 }
 
 static int launch(const BatchHeader& h, const GemvDesc* table_dev, const GemvDesc& one, void* stream) {
@@ -120,6 +129,7 @@ int bitcos_batch_build(int32_t count, const bitcos_layout* layouts, const void* 
   bitcos::GemvDesc* descs =
       reinterpret_cast<bitcos::GemvDesc*>(static_cast<uint8_t*>(table) + sizeof(bitcos::BatchHeader));
   int64_t units = 0;
+  int step_rows = 0;
   h.unit_is_step = 1;
   for (int32_t i = 0; i < count; ++i) {
     const bitcos_layout* L = &layouts[i];
@@ -136,9 +146,15 @@ int bitcos_batch_build(int32_t count, const bitcos_layout* layouts, const void* 
     st = bitcos::make_desc(L, blobs_dev[i], x_dev[i], xscale_dev ? xscale_dev[i] : nullptr, y_dev[i],
                            x_dtype, y_mode, &descs[i]);
     if (st) return st;
+    if (h.format != BITCOS_FMT_BITCOS || rows % descs[i].unit_rows) h.unit_is_step = 0;
+    step_rows = rows;
+  }
+  // The streaming kernel counts every GEMV in wave steps; the general kernel
+  // in the layout's units.
+  for (int32_t i = 0; i < count; ++i) {
+    if (h.unit_is_step) bitcos::to_step_units(&descs[i], step_rows);
     descs[i].unit_begin = units;
     units += descs[i].units;
-    if (descs[i].unit_rows != rows) h.unit_is_step = 0;
   }
   h.total_units = units;
   memcpy(table, &h, sizeof(h));

@@ -1,5 +1,5 @@
-// BITCOS GEMV, streaming kernel for layouts whose unit is one wave step
-// (unit_rows == 64 / SEG rows, the library default).
+// BITCOS GEMV, streaming kernel for layouts whose unit divides one wave step
+// of 64 / SEG rows (the library default is one sign offset per row).
 //
 // With one stored sign offset per step, the step's whole sign range
 // [off[u], off[u+1]) is known before its presence words arrive, so nothing
@@ -63,6 +63,7 @@ struct FastGen {
   int U, Uend;           // the launch's units fit in 31 bits (checked on the host)
   int begin, end;        // unit range of GEMV di in the launch
   const uint32_t* offs;  // its unit offsets
+  int stride, last;      // offset entries per step; index of the last entry
 
   __device__ __forceinline__ void enter(const KernelArgs& a, int d) {
     di = __builtin_amdgcn_readfirstlane(d);
@@ -70,6 +71,8 @@ struct FastGen {
     begin = static_cast<int>(g.unit_begin);
     end = static_cast<int>(g.unit_begin + g.units);
     offs = g.offsets;
+    stride = g.offset_stride;
+    last = g.offset_last;
   }
 
   __device__ __forceinline__ FastStep next(const KernelArgs& a) {
@@ -86,8 +89,8 @@ struct FastGen {
     const int u = U - begin;
     s.di = di;
     s.row0 = u * R;
-    s.off0 = cp_u32(offs)[u];
-    s.off1 = cp_u32(offs)[u + 1];
+    s.off0 = cp_u32(offs)[u * stride];
+    s.off1 = cp_u32(offs)[min((u + 1) * stride, last)];
     ++U;
     return s;
   }

@@ -90,7 +90,7 @@ extern "C" int bitcos_gemv(const bitcos_layout* L, const void* blob_dev, int32_t
   int rows = 0;
   st = bitcos::tile_for(L, x_dtype, &h.per_lane, &h.seg, &rows);
   if (st) return st;
+  h.unit_is_step = bitcos::to_step_units(&d, rows);
   h.total_units = d.units;
-  h.unit_is_step = d.unit_rows == rows;
   return bitcos::launch_bitcos(h, nullptr, d, stream);
 }

@@ -57,12 +57,13 @@ inline bool bitcos_tile(int k, bool bf16, Tile* t) {
   return choose_tile(k / 32, bf16 ? kMaxWordsBf16 : kMaxWordsI8, t);
 }
 
-// Default rows per sign offset: one wave step.
+// Default rows per sign offset: one, so every kernel (any rows per wave step,
+// the batched MFMA kernel's 16-row tiles) finds each row's entry point; 4
+// bytes of metadata per row.
 inline int bitcos_default_unit_rows(int n, int k) {
-  Tile t;
-  if (!bitcos_tile(k, false, &t)) return 1;
   (void)n;
-  return t.rows;
+  (void)k;
+  return 1;
 }
 
 // BITCOS layout (section placement, sizes, payload bits) of an n x k matrix
