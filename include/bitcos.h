@@ -88,6 +88,8 @@ extern "C" {
 #define BITCOS_X_I8 1         /* activations int8 [m][K]                 */
 #define BITCOS_X_BF16 2       /* activations bfloat16 bit patterns [m][K] */
 
+#define BITCOS_MAX_M 16        /* most activation rows per GEMV call      */
+
 #define BITCOS_Y_F32 1        /* y float32 [m][N], scaled                 */
 #define BITCOS_Y_I32_RAW 2    /* y int32 [m][N] = sum_k W x, unscaled (int8 x only) */
 
@@ -140,7 +142,11 @@ int bitcos_unpack(const bitcos_layout* L, const void* blob, size_t blob_bytes, i
 
 /* bitcos_gemv: y = (S (.) W) x on the device, enqueued on `stream`.
  *   blob_dev  device copy of the packed blob (L->total_bytes bytes).
- *   m         number of activation rows; 1 (batch-1 decode).
+ *   m         number of activation rows, 1..BITCOS_MAX_M.  m = 1 is batch-1
+ *             decode.  2 <= m <= 16 runs the small-batch kernel (every
+ *             decoded weight multiplied against all m rows on the matrix
+ *             cores) when the layout has one sign offset per row and
+ *             k % 128 == 0; other layouts run m batch-1 launches.
  *   x_dev     device activations [m][k]: int8 (BITCOS_X_I8) or bf16 bits
  *             (BITCOS_X_BF16), row-major.
  *   xscale_dev  NULL (a = 1) or device fp32 [m][k/128] per-group activation
@@ -150,7 +156,8 @@ int bitcos_unpack(const bitcos_layout* L, const void* blob, size_t blob_bytes, i
  * int8 x accumulates exactly in int32 per group and applies the scale once per
  * group in fp32; with one scale per tensor and no xscale the full int32 row
  * sum is multiplied once.  bf16 x accumulates in fp32.
- * Errors: E_ARG, E_UNSUPPORTED (m, dtype or shape without a kernel), E_HIP. */
+ * Errors: E_ARG (also m outside 1..BITCOS_MAX_M), E_UNSUPPORTED (dtype or
+ * shape without a kernel), E_HIP. */
 int bitcos_gemv(const bitcos_layout* L, const void* blob_dev, int32_t m, const void* x_dev,
                 int32_t x_dtype, const float* xscale_dev, void* y_dev, int32_t y_mode,
                 void* stream);
@@ -183,22 +190,26 @@ int bit2_gemv(const bitcos_layout* L, const void* blob_dev, int32_t m, const voi
  * ONE tile (bitcos_describe reports per_lane and seg_lanes) as a single
  * persistent launch: every wave takes a contiguous range of the list's work
  * units.  Each GEMV keeps the single-call semantics above (its own x, xscale
- * and y; y overwritten; m = 1).
+ * and y; y overwritten), with the same number m of activation rows.
  *
  * bitcos_batch_bytes: bytes of a batch table for `count` GEMVs (0 if count < 1).
  *
  * bitcos_batch_build: fill a host table (table_bytes >= bitcos_batch_bytes)
- * for `count` GEMVs: layouts[i] (host), blobs_dev[i], x_dev[i], y_dev[i]
- * (device pointers), xscale_dev NULL or an array of per-GEMV device
- * pointers (entries may be NULL).  The table records the device pointers:
- * they must stay valid while the table is in use.  Errors: E_ARG, E_SPACE,
- * E_UNSUPPORTED (mixed formats or tiles: build one batch per tile).
+ * for `count` GEMVs of m activation rows each (1..BITCOS_MAX_M): layouts[i]
+ * (host), blobs_dev[i], x_dev[i] ([m][k]), y_dev[i] ([m][n]) (device
+ * pointers), xscale_dev NULL or an array of per-GEMV device pointers
+ * ([m][k/128]; entries may be NULL).  The table records the device pointers:
+ * they must stay valid while the table is in use.  m > 1 takes BITCOS
+ * layouts with one sign offset per row and k % 128 == 0 (the small-batch
+ * kernel).  Errors: E_ARG, E_SPACE, E_UNSUPPORTED (mixed formats or tiles:
+ * build one batch per tile; m > 1 with another layout).
  *
  * bitcos_gemv_batch: copy of the table in device memory (16-byte aligned,
  * unchanged since built) plus the host table it was copied from; enqueues
  * one launch on `stream`.  Errors: E_ARG, E_UNSUPPORTED, E_HIP. */
 size_t bitcos_batch_bytes(int32_t count);
-int bitcos_batch_build(int32_t count, const bitcos_layout* layouts, const void* const* blobs_dev,
+int bitcos_batch_build(int32_t count, int32_t m, const bitcos_layout* layouts,
+                       const void* const* blobs_dev,
                        const void* const* x_dev, const float* const* xscale_dev,
                        void* const* y_dev, int32_t x_dtype, int32_t y_mode, void* table,
                        size_t table_bytes);

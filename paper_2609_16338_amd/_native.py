@@ -24,6 +24,7 @@ SEC_BITMAP, SEC_SIGNS, SEC_OFFSETS, SEC_SCALES = 0, 1, 2, 3
 SEC_CODES = 0
 X_I8, X_BF16 = 1, 2
 Y_F32, Y_I32_RAW = 1, 2
+MAX_M = 16  # most activation rows per GEMV call
 LAYOUT_VERSION = 1
 
 
@@ -91,7 +92,7 @@ SIGNATURES = {
     "bitcos_describe": (ctypes.c_int, [_LP, _I32, _I32, ctypes.POINTER(LaunchInfo)]),
     "bitcos_quantize_act": (ctypes.c_int, [_P, _I32, _I32, _P, _P, _P]),
     "bitcos_batch_bytes": (ctypes.c_size_t, [_I32]),
-    "bitcos_batch_build": (ctypes.c_int, [_I32, _P, _P, _P, _P, _P, _I32, _I32, _P, _SZ]),
+    "bitcos_batch_build": (ctypes.c_int, [_I32, _I32, _P, _P, _P, _P, _P, _I32, _I32, _P, _SZ]),
     "bitcos_gemv_batch": (ctypes.c_int, [_P, _P, _P]),
     "bitcos_plan_device_workspace": (ctypes.c_size_t, [_I32]),
     "bitcos_plan_device": (ctypes.c_int, [_P, _I32, _I32, _I32, _I32, _P, _SZ, _LP, _P]),

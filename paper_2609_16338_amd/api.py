@@ -241,7 +241,9 @@ class Batch:
     """A list of GEMVs of one format and tile, run as one persistent launch.
 
     Holds the host table and its device copy; the device buffers it points to
-    (blobs, activations, outputs) must outlive it.
+    (blobs, activations, outputs) must outlive it.  Every GEMV takes the same
+    number m of activation rows: xs[i] is [m, k] (or [k] for m = 1) and ys[i]
+    [m, n]; m > 1 runs the small-batch kernel.
     """
 
     def __init__(self, layouts, blobs_dev, xs, ys, xscales=None, y_mode: int = Y_F32):
@@ -250,13 +252,14 @@ class Batch:
         if not (count == len(blobs_dev) == len(xs) == len(ys)) or count < 1:
             raise ValueError("layouts, blobs, xs and ys must have the same non-zero length")
         x_dtype = X_I8 if xs[0].dtype == torch.int8 else X_BF16
+        m = xs[0].shape[0] if xs[0].dim() == 2 else 1
         arr = (Layout * count)(*layouts)
         for L, b, x, y in zip(layouts, blobs_dev, xs, ys):
-            _check_gemv_buffers(L, b, x, y, None, y_mode)
+            _check_gemv_buffers(L, b, x, y, None, y_mode, m)
         if xscales is not None:
             for L, xs_ in zip(layouts, xscales):
                 if xs_ is not None:
-                    _check_xscale(L, xs_, 1)
+                    _check_xscale(L, xs_, m)
         P = ctypes.c_void_p
         blobs = (P * count)(*[b.data_ptr() for b in blobs_dev])
         xp = (P * count)(*[x.data_ptr() for x in xs])
@@ -264,10 +267,11 @@ class Batch:
         sp = None if xscales is None else (P * count)(*[0 if s is None else s.data_ptr() for s in xscales])
         nbytes = N.lib().bitcos_batch_bytes(count)
         self.host = np.zeros(nbytes, dtype=np.uint8)
-        N.check(N.lib().bitcos_batch_build(count, arr, blobs, xp, sp, yp, x_dtype, y_mode,
+        N.check(N.lib().bitcos_batch_build(count, m, arr, blobs, xp, sp, yp, x_dtype, y_mode,
                                            _ptr(self.host), nbytes), "bitcos_batch_build")
         self.dev = torch.from_numpy(self.host).cuda()
         self.count = count
+        self.m = m
         self._keep = (layouts, blobs_dev, xs, ys, xscales)
 
     def run(self, stream=None):
@@ -275,17 +279,17 @@ class Batch:
                                           _stream_handle(stream)), "bitcos_gemv_batch")
 
 
-def _check_gemv_buffers(L, blob_dev, x, y, xscale, y_mode):
+def _check_gemv_buffers(L, blob_dev, x, y, xscale, y_mode, m=1):
     import torch
     for t, nm in ((blob_dev, "blob"), (x, "x"), (y, "y")):
         if not t.is_cuda or not t.is_contiguous():
             raise ValueError(f"{nm} must be a contiguous cuda tensor")
     if blob_dev.dtype != torch.uint8 or blob_dev.numel() < L.total_bytes:
         raise ValueError("blob_dev must be uint8 with at least total_bytes elements")
-    if x.numel() != L.k or x.dtype not in (torch.int8, torch.bfloat16):
-        raise ValueError("x must be int8 or bfloat16 with k elements")
+    if x.numel() != m * L.k or x.dtype not in (torch.int8, torch.bfloat16):
+        raise ValueError("x must be int8 or bfloat16 with m * k elements")
     want_y = torch.int32 if y_mode == Y_I32_RAW else torch.float32
-    if y.dtype != want_y or y.numel() != L.n:
+    if y.dtype != want_y or y.numel() != m * L.n:
         raise ValueError("y has the wrong dtype or size")
 
 

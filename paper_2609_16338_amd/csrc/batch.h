@@ -59,7 +59,9 @@ struct BatchHeader {
   int32_t seg;
   int64_t total_units;
   int32_t unit_is_step;  // every GEMV's unit is one wave step (BITCOS streaming kernel)
-  int32_t reserved[21];
+  int32_t m;             // activation rows (> 1: the small-batch MFMA kernel)
+  int32_t any_xscale;    // some GEMV has activation scales
+  int32_t reserved[19];
 };
 static_assert(sizeof(BatchHeader) == 128, "BatchHeader is 128 bytes");
 
@@ -72,6 +74,36 @@ inline size_t batch_bytes(int32_t count) {
 // each format's kernels.
 int launch_bitcos(const BatchHeader& h, const GemvDesc* table_dev, const GemvDesc& one, void* stream);
 int launch_fixed(const BatchHeader& h, const GemvDesc* table_dev, const GemvDesc& one, void* stream);
+int launch_bitcos_mfma(const BatchHeader& h, const GemvDesc* table_dev, const GemvDesc& one, void* stream);
+
+// Small-batch (m > 1) BITCOS kernel: rows per work unit, and the layouts it
+// runs (one sign offset per row, whole 128-weight groups).
+constexpr int kMfmaUnitRows = 32;
+inline bool mfma_layout_ok(const bitcos_layout* L) {
+  return L->format == BITCOS_FMT_BITCOS && L->unit_rows == 1 && L->k % 128 == 0;
+}
+
+// m activation rows as m batch-1 calls of `gemv` (row i: x + i k, xscale +
+// i k / 128, y + i n), for layouts the small-batch kernel does not take.
+// The first call validates everything the others would, so an error
+// enqueues nothing.
+using GemvEntry = int (*)(const bitcos_layout*, const void*, int32_t, const void*, int32_t, const float*, void*,
+                          int32_t, void*);
+inline int gemv_rows(GemvEntry gemv, const bitcos_layout* L, const void* blob_dev, int32_t m, const void* x_dev,
+                     int32_t x_dtype, const float* xscale_dev, void* y_dev, int32_t y_mode, void* stream) {
+  const size_t xrow = static_cast<size_t>(L->k) * (x_dtype == BITCOS_X_BF16 ? 2u : 1u);
+  for (int32_t i = 0; i < m; ++i) {
+    const void* x = x_dev ? static_cast<const uint8_t*>(x_dev) + i * xrow : nullptr;
+    const float* xs = xscale_dev ? xscale_dev + static_cast<size_t>(i) * (L->k / 128) : nullptr;
+    void* y = y_dev ? static_cast<uint8_t*>(y_dev) + static_cast<size_t>(i) * L->n * 4u : nullptr;
+    const int st = gemv(L, blob_dev, 1, x, x_dtype, xs, y, y_mode, stream);
+    if (st) return st;
+  }
+  return BITCOS_OK;
+}
+
+// Count a descriptor's units as the small-batch kernel's units.
+inline void to_mfma_units(GemvDesc* d) { d->units = (d->n + kMfmaUnitRows - 1) / kMfmaUnitRows; }
 
 // Tile (per-lane units, lanes per row) the given layout runs with.
 int tile_for(const bitcos_layout* L, int32_t x_dtype, int* per_lane, int* seg, int* rows);
@@ -80,8 +112,9 @@ int tile_for(const bitcos_layout* L, int32_t x_dtype, int* per_lane, int* seg, i
 // streaming BITCOS kernel; possible when the layout's unit divides the step.
 bool to_step_units(GemvDesc* d, int rows);
 
-// Fill one descriptor from a layout and device pointers (unit_begin = 0).
+// Fill one descriptor from a layout and device pointers (unit_begin = 0);
+// m activation rows ([m][k] in, [m][n] out).
 int make_desc(const bitcos_layout* L, const void* blob_dev, const void* x_dev, const float* xscale_dev,
-              void* y_dev, int32_t x_dtype, int32_t y_mode, GemvDesc* d);
+              void* y_dev, int32_t x_dtype, int32_t y_mode, GemvDesc* d, int32_t m = 1);
 
 }  // namespace bitcos

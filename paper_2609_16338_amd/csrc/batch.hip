@@ -47,7 +47,8 @@ static int check_layout(const bitcos_layout* L) {
 }
 
 int make_desc(const bitcos_layout* L, const void* blob_dev, const void* x_dev, const float* xscale_dev,
-              void* y_dev, int32_t x_dtype, int32_t y_mode, GemvDesc* d) {
+              void* y_dev, int32_t x_dtype, int32_t y_mode, GemvDesc* d, int32_t m) {
+  if (m < 1 || m > BITCOS_MAX_M) return BITCOS_E_ARG;
   int st = check_layout(L);
   if (st) return st;
   if (x_dtype != BITCOS_X_I8 && x_dtype != BITCOS_X_BF16) return BITCOS_E_ARG;
@@ -56,8 +57,10 @@ int make_desc(const bitcos_layout* L, const void* blob_dev, const void* x_dev, c
   if (!blob_dev || !x_dev || !y_dev) return BITCOS_E_ARG;
   if (xscale_dev && L->k % 128) return BITCOS_E_ARG;
   int per_lane = 0, seg = 0, rows = 0;
-  st = tile_for(L, x_dtype, &per_lane, &seg, &rows);
-  if (st) return st;
+  if (m == 1 || !mfma_layout_ok(L)) {  // the small-batch kernel has no tile limit on K
+    st = tile_for(L, x_dtype, &per_lane, &seg, &rows);
+    if (st) return st;
+  }
   memset(d, 0, sizeof(*d));
   const uint8_t* blob = static_cast<const uint8_t*>(blob_dev);
   d->sec0 = blob + L->sec_off[0];
@@ -71,8 +74,11 @@ int make_desc(const bitcos_layout* L, const void* blob_dev, const void* x_dev, c
   if (L->sec_bytes[0] >= 0x80000000ull || L->total_bytes >= 0x80000000ull) return BITCOS_E_UNSUPPORTED;
   d->sec0_bytes = static_cast<uint32_t>(L->sec_bytes[0]);
   d->scales_bytes = static_cast<uint32_t>(L->sec_bytes[BITCOS_SEC_SCALES]);
-  d->x_bytes = static_cast<uint32_t>(L->k) * (x_dtype == BITCOS_X_BF16 ? 2u : 1u);
-  d->y_bytes = static_cast<uint32_t>(L->n) * 4u;
+  const uint64_t xb = static_cast<uint64_t>(m) * L->k * (x_dtype == BITCOS_X_BF16 ? 2u : 1u);
+  const uint64_t yb = static_cast<uint64_t>(m) * L->n * 4u;
+  if (xb >= 0x80000000ull || yb >= 0x80000000ull) return BITCOS_E_UNSUPPORTED;
+  d->x_bytes = static_cast<uint32_t>(xb);
+  d->y_bytes = static_cast<uint32_t>(yb);
   d->mode = (L->group == 128 ? kModeGrouped : 0) | (xscale_dev ? kModeXscale : 0) |
             (y_mode == BITCOS_Y_I32_RAW ? kModeRaw : 0);
   if (L->format == BITCOS_FMT_BITCOS) {
@@ -101,8 +107,34 @@ bool to_step_units(GemvDesc* d, int rows) {
 }
 
 static int launch(const BatchHeader& h, const GemvDesc* table_dev, const GemvDesc& one, void* stream) {
+  if (h.m > 1) return launch_bitcos_mfma(h, table_dev, one, stream);
   return h.format == BITCOS_FMT_BITCOS ? launch_bitcos(h, table_dev, one, stream)
                                        : launch_fixed(h, table_dev, one, stream);
+}
+
+// Batch table for m > 1 (the small-batch kernel; BITCOS layouts it runs only).
+static int build_small_batch(int32_t count, int32_t m, const bitcos_layout* layouts,
+                             const void* const* blobs_dev, const void* const* x_dev,
+                             const float* const* xscale_dev, void* const* y_dev, BatchHeader* h,
+                             GemvDesc* descs) {
+  int64_t units = 0;
+  for (int32_t i = 0; i < count; ++i) {
+    const bitcos_layout* L = &layouts[i];
+    if (L->format != BITCOS_FMT_BITCOS) return L->format == BITCOS_FMT_TRIT5 || L->format == BITCOS_FMT_BIT2
+                                                   ? BITCOS_E_UNSUPPORTED
+                                                   : BITCOS_E_ARG;
+    const float* xs = xscale_dev ? xscale_dev[i] : nullptr;
+    int st = make_desc(L, blobs_dev[i], x_dev[i], xs, y_dev[i], h->x_dtype, h->y_mode, &descs[i], m);
+    if (st) return st;
+    if (!mfma_layout_ok(L)) return BITCOS_E_UNSUPPORTED;
+    if (xs) h->any_xscale = 1;
+    to_mfma_units(&descs[i]);
+    descs[i].unit_begin = units;
+    units += descs[i].units;
+  }
+  if (units >= (int64_t(1) << 31)) return BITCOS_E_UNSUPPORTED;
+  h->total_units = units;
+  return BITCOS_OK;
 }
 
 }  // namespace bitcos
@@ -113,10 +145,11 @@ size_t bitcos_batch_bytes(int32_t count) {
   return count < 1 ? 0 : bitcos::batch_bytes(count);
 }
 
-int bitcos_batch_build(int32_t count, const bitcos_layout* layouts, const void* const* blobs_dev,
+int bitcos_batch_build(int32_t count, int32_t m, const bitcos_layout* layouts, const void* const* blobs_dev,
                        const void* const* x_dev, const float* const* xscale_dev, void* const* y_dev,
                        int32_t x_dtype, int32_t y_mode, void* table, size_t table_bytes) {
   if (count < 1 || !layouts || !blobs_dev || !x_dev || !y_dev || !table) return BITCOS_E_ARG;
+  if (m < 1 || m > BITCOS_MAX_M) return BITCOS_E_ARG;
   if (table_bytes < bitcos::batch_bytes(count)) return BITCOS_E_SPACE;
   bitcos::BatchHeader h;
   memset(&h, 0, sizeof(h));
@@ -126,8 +159,15 @@ int bitcos_batch_build(int32_t count, const bitcos_layout* layouts, const void* 
   h.count = count;
   h.x_dtype = x_dtype;
   h.y_mode = y_mode;
+  h.m = m;
   bitcos::GemvDesc* descs =
       reinterpret_cast<bitcos::GemvDesc*>(static_cast<uint8_t*>(table) + sizeof(bitcos::BatchHeader));
+  if (m > 1) {
+    int st = bitcos::build_small_batch(count, m, layouts, blobs_dev, x_dev, xscale_dev, y_dev, &h, descs);
+    if (st) return st;
+    memcpy(table, &h, sizeof(h));
+    return BITCOS_OK;
+  }
   int64_t units = 0;
   int step_rows = 0;
   h.unit_is_step = 1;
@@ -166,6 +206,7 @@ int bitcos_gemv_batch(const void* table_host, const void* table_dev, void* strea
   bitcos::BatchHeader h;
   memcpy(&h, table_host, sizeof(h));
   if (h.magic != bitcos::kBatchMagic || h.version != BITCOS_LAYOUT_VERSION || h.count < 1) return BITCOS_E_ARG;
+  if (h.m < 1 || h.m > BITCOS_MAX_M) return BITCOS_E_ARG;
   if (reinterpret_cast<uintptr_t>(table_dev) % 16) return BITCOS_E_ARG;
   const bitcos::GemvDesc* descs = reinterpret_cast<const bitcos::GemvDesc*>(
       static_cast<const uint8_t*>(table_dev) + sizeof(bitcos::BatchHeader));
@@ -176,9 +217,20 @@ int bitcos_gemv_batch(const void* table_host, const void* table_dev, void* strea
 
 int bitcos_describe(const bitcos_layout* L, int32_t m, int32_t x_dtype, bitcos_launch_info* out) {
   if (!L || !out) return BITCOS_E_ARG;
-  if (m != 1) return m < 1 ? BITCOS_E_ARG : BITCOS_E_UNSUPPORTED;
+  if (m < 1 || m > BITCOS_MAX_M) return BITCOS_E_ARG;
   int st = bitcos::check_layout(L);
   if (st) return st;
+  if (x_dtype != BITCOS_X_I8 && x_dtype != BITCOS_X_BF16) return BITCOS_E_ARG;
+  if (m > 1 && bitcos::mfma_layout_ok(L)) {  // small-batch kernel: 4 lanes per row, one word each per group
+    const int64_t units = (L->n + bitcos::kMfmaUnitRows - 1) / bitcos::kMfmaUnitRows;
+    out->per_lane = 1;
+    out->seg_lanes = 4;
+    out->rows_per_step = bitcos::kMfmaUnitRows;
+    out->lanes_used = 4;
+    out->waves = units;
+    out->workgroups = (units + 7) / 8;
+    return BITCOS_OK;
+  }
   int per_lane = 0, seg = 0, rows = 0;
   st = bitcos::tile_for(L, x_dtype, &per_lane, &seg, &rows);
   if (st) return st;

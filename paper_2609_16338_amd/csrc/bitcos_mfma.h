@@ -1,0 +1,443 @@
+// BITCOS GEMV for a small batch of activation rows (2 <= M <= 16) on the
+// matrix cores.  Decode cost per weight is the same at any batch size, so a
+// batch of M activation rows multiplies every decoded weight M times: one
+// MFMA takes a decoded weight tile against all (up to 16) rows at once.
+//
+// Work unit: 32 output rows (two 16-row MFMA tiles) over the whole of K; a
+// wave walks its units in steps of four 128-weight scale groups.
+//   * Lane l works on row n = l % 16 of each tile and, in every group, on its
+//     32-weight word g = l / 16, so the four lane groups of a row cover one
+//     group together and an MFMA never mixes two scale groups.
+//   * B operand (weights, K x 16 rows): per presence byte of the lane's word
+//     the 8 weights come out of two LDS table lookups keyed by the presence
+//     byte m and the next 8 compact sign bits s, combined by v_perm_b32
+//     (Eq. (2) w = p - 2n, with the deposit of Sec. II-B done by the table):
+//     int8 +-1 bytes for v_mfma_i32_16x16x64_i8, bf16 +-0.5 for
+//     v_mfma_f32_16x16x32_bf16 (the 0.5 is undone exactly at the end).
+//   * A operand (activations, 16 batch rows x K): lane (m, g) holds batch row
+//     m's activations at the positions its B partner decodes; rows m >= M
+//     read zero through the buffer range check, so one kernel serves every M.
+//   * C (16 batch rows x 16 output rows): lane l holds batch rows
+//     4 (l / 16) + i of output row l % 16.  Every group's C is scaled into
+//     fp32 accumulators (fp16 group scale x activation scale, Sec. II-C), or
+//     summed exactly in int32 when the scale is per tensor.
+// Sign cursors: every row's entry comes from its offset entry (one per row);
+// in a step the four lanes of a row exchange their words' popcounts (one
+// byte per group) to place each word.  A row's signs for one step (at most
+// 512 bits, starting anywhere in a dword) are fetched as 20 dwords, staged
+// in the wave's LDS block and read as 64-bit windows.
+// Pipeline: the presence words, group scales and sign dwords of step t+1 are
+// issued at the start of step t (the sign range of step t+1 follows from the
+// popcounts of step t).  Activations of step t+1 are issued during step t,
+// group by group as step t's MFMAs release their registers, so that waiting
+// for them never waits on a prefetch issued after them.
+#pragma once
+
+#include "bitcos_kernel.h"
+
+namespace bitcos_k {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef int i32x4_t __attribute__((ext_vector_type(4)));
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+
+constexpr int kMfmaTile = 16;                   // output rows per MFMA tile
+constexpr int kMfmaRT = 2;                      // tiles per work unit
+constexpr int kMfmaRows = kMfmaTile * kMfmaRT;  // rows per work unit
+constexpr int kMfmaThreads = 512;
+constexpr int kMfmaMaxBatch = 16;
+constexpr int kSignStride = 21;                 // LDS dwords per staged row (20 used; odd spreads banks)
+
+// int8 weights in deposit form: exp[e] byte b = rank of bit b among the set
+// bits of e if bit b is set, else 0x0C (v_perm_b32 writes 0); tsg[e] byte q =
+// 0xFF if bit q of e is set, else 0x01.  perm(tsg[s], exp[m]) is then the 8
+// weights of presence byte m with compact signs s, as int8.
+struct DepTablesI8 {
+  uint2 exp[256 * Cfg<false>::kCopies];
+  uint2 tsg[256 * Cfg<false>::kCopies];
+};
+
+template <bool BF16>
+struct MfmaTables {
+  using type = DepTablesI8;
+};
+template <>
+struct MfmaTables<true> {
+  using type = Tables<true>;
+};
+
+__device__ __forceinline__ void build_mfma_tables(DepTablesI8& t, int tid, int nthreads) {
+  constexpr int NC = Cfg<false>::kCopies;
+  for (int idx = tid; idx < 256 * NC; idx += nthreads) {
+    const int e = idx & 255;
+    const int c = idx >> 8;
+    uint32_t ex[8], g[8];
+    uint32_t r = 0;
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+      const bool on = (e >> b) & 1;
+      ex[b] = on ? r : 0x0Cu;
+      r += on;
+      g[b] = on ? 0xFFu : 0x01u;
+    }
+    t.exp[e * NC + c] = make_uint2(bytes4(ex[0], ex[1], ex[2], ex[3]), bytes4(ex[4], ex[5], ex[6], ex[7]));
+    t.tsg[e * NC + c] = make_uint2(bytes4(g[0], g[1], g[2], g[3]), bytes4(g[4], g[5], g[6], g[7]));
+  }
+}
+__device__ __forceinline__ void build_mfma_tables(Tables<true>& t, int tid, int n) { build_tables<true>(t, tid, n); }
+
+__device__ __forceinline__ u32x4_t ld128(rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+
+// Wave-uniform position of one step.
+struct MStep {
+  int di;      // descriptor
+  int unit;    // unit within the GEMV
+  int c;       // step within the unit
+  bool last;   // last step of the unit
+  bool valid;
+};
+
+template <bool BF16, bool XS, bool TABLE>
+__global__ void __launch_bounds__(kMfmaThreads) bitcos_mfma_kernel(const KernelArgs a) {
+  constexpr int NC = Cfg<BF16>::kCopies;
+  constexpr int WPB = kMfmaThreads / kWave;
+  constexpr int RT = kMfmaRT;
+  constexpr int ELEM = BF16 ? 2 : 1;  // bytes per activation
+  constexpr int NA = BF16 ? 4 : 2;    // MFMAs (16-byte activation pieces) per word
+  using CV = typename std::conditional<BF16, f32x4_t, i32x4_t>::type;
+
+  __shared__ typename MfmaTables<BF16>::type tab;
+  __shared__ uint32_t sstage[WPB * kMfmaRows * kSignStride];
+  build_mfma_tables(tab, threadIdx.x, kMfmaThreads);
+  __syncthreads();
+
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wave = __builtin_amdgcn_readfirstlane(blockIdx.x * WPB + wv);
+  const int total = static_cast<int>(a.total_units);
+  const int nwaves = static_cast<int>(gridDim.x) * WPB;
+  const int per = (total + nwaves - 1) / nwaves;
+  const int U0 = per * wave;
+  const int U1 = min(U0 + per, total);
+  if (U0 >= U1) return;
+
+  const int nr = lane & 15;
+  const int g = lane >> 4;
+  const int cp = lane & (NC - 1);
+  uint32_t* const stage = sstage + wv * (kMfmaRows * kSignStride);
+
+  // ---- fetch side: the GEMV whose step is being fetched
+  int fdi = 0, fbeg = 0, fend = 0, fC = 1, fG = 1, fk = 0, fupr = 0;
+  rsrc_t rb = make_rsrc(nullptr, 0), rg = rb, rs = rb, rx = rb, rxs = rb;
+  auto fetch_enter = [&](int d) {
+    fdi = __builtin_amdgcn_readfirstlane(d);
+    const auto& D = desc_at<TABLE>(a, fdi);
+    fbeg = static_cast<int>(D.unit_begin);
+    fend = static_cast<int>(D.unit_begin + D.units);
+    fG = D.ngroups;
+    fC = (fG + 3) >> 2;
+    fk = D.upr * 32;
+    fupr = D.upr;
+    rb = make_rsrc(D.sec0, D.sec0_bytes);
+    rg = make_rsrc(D.signs, D.signs_bytes);
+    rs = make_rsrc(D.scales, (D.mode & kModeGrouped) ? D.scales_bytes : 0u);
+    rx = make_rsrc(D.x, D.x_bytes);
+    const bool xs = XS && (D.mode & kModeXscale);
+    rxs = make_rsrc(xs ? D.xscale : nullptr, xs ? D.x_bytes / (32u * ELEM) : 0u);
+  };
+  // Sign offsets of the lane's rows in unit U of the launch (U in the GEMV
+  // being fetched or the next one).
+  auto unit_offsets = [&](int U, uint32_t (&o)[RT]) {
+    const bool in = U < U1;
+    const int d = (U < fend) ? fdi : min(fdi + 1, a.count - 1);
+    const auto& D = desc_at<TABLE>(a, d);
+    const rsrc_t ro = make_rsrc(D.offsets, static_cast<uint32_t>(D.n + 1) * 4u);
+    const int row0 = (U - static_cast<int>(D.unit_begin)) * kMfmaRows;
+#pragma unroll
+    for (int r = 0; r < RT; ++r)
+      o[r] = ld32(ro, in ? static_cast<uint32_t>(row0 + kMfmaTile * r + nr) * 4u : kOOB);
+  };
+
+  {
+    int lo = 0;
+    if constexpr (TABLE) {  // last descriptor with unit_begin <= U0
+      int hi = a.count;
+      while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (((CDesc*)a.table)[mid].unit_begin <= U0) lo = mid; else hi = mid;
+      }
+    }
+    fetch_enter(lo);
+  }
+
+  // Step data: presence words, fp16 group scales and sign dwords of the
+  // lane's row in each tile, and the row's sign position at the step start.
+  struct Slot {
+    uint32_t P[RT][4];
+    uint32_t SC[RT][4];
+    u32x4_t SA[RT];
+    uint32_t SB[RT];
+    uint32_t pos[RT];
+  };
+  auto issue = [&](const MStep& s, Slot& d) {
+    const int c = s.valid ? s.c : 0;
+    const int row0 = s.unit * kMfmaRows;
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+      const uint32_t row = static_cast<uint32_t>(row0 + kMfmaTile * r + nr);
+      const uint32_t pbase = (row * fupr + 16u * c + g) * 4u;
+      const uint32_t sbase = (row * fG + 4u * c) * 2u;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const bool ok = s.valid && 4 * c + q < fG;
+        d.P[r][q] = ld32(rb, ok ? pbase + 16u * q : kOOB);
+        d.SC[r][q] = ld16(rs, ok ? sbase + 2u * q : kOOB);
+      }
+      const uint32_t sdw = d.pos[r] >> 5;
+      d.SA[r] = ld128(rg, s.valid ? (sdw + 4u * g) * 4u : kOOB);
+      d.SB[r] = ld32(rg, s.valid ? (sdw + 16u + g) * 4u : kOOB);
+    }
+  };
+  // Activations of group q of a step: 32 of batch row nr at the lane's word
+  // (and with XS, the activation scales of batch rows 4 g + i).
+  u32x4_t A[4][NA];
+  float XA[4][4];
+  auto issue_x = [&](const MStep& s, int q) {
+    const int gi = 4 * (s.valid ? s.c : 0) + q;
+    const bool ok = s.valid && gi < fG;
+    const uint32_t off = ok ? (static_cast<uint32_t>(nr * fk) + 128u * gi + 32u * g) * ELEM : kOOB;
+#pragma unroll
+    for (int j = 0; j < NA; ++j) A[q][j] = ld128(rx, off + 16u * j);
+    if constexpr (XS) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        XA[q][i] = __builtin_bit_cast(
+            float, ld32(rxs, ok ? (static_cast<uint32_t>((4 * g + i) * fG) + gi) * 4u : kOOB));
+    }
+  };
+  auto advance = [&](const MStep& s) {
+    MStep n = s;
+    if (s.c + 1 < fC) {
+      n.c = s.c + 1;
+    } else {
+      const int U = fbeg + s.unit + 1;
+      n.valid = U < U1;
+      if (n.valid && U >= fend) fetch_enter(fdi + 1);
+      n.di = fdi;
+      n.unit = U - fbeg;
+      n.c = 0;
+    }
+    n.last = n.c + 1 == fC;
+    return n;
+  };
+
+  // ---- decode side: output of the GEMV whose step is being decoded
+  int ddi = -1, dn = 0;
+  // scaled: per-group fp32 accumulation; dxs: the GEMV has activation scales
+  bool grouped = false, raw = false, scaled = false, dxs = false;
+  float tscale = 0.0f;
+  rsrc_t ry = make_rsrc(nullptr, 0);
+
+  // Accumulators: batch rows 4 g + i of output row nr of each tile.
+  float acc[RT][4];
+  int iacc[RT][4];
+#pragma unroll
+  for (int r = 0; r < RT; ++r)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      acc[r][i] = 0.0f;
+      iacc[r][i] = 0;
+    }
+
+  // ---- prologue
+  MStep fs;
+  fs.di = fdi;
+  fs.unit = U0 - fbeg;
+  fs.c = 0;
+  fs.last = fC == 1;
+  fs.valid = true;
+  Slot cur, nxt;
+  uint32_t offn[RT];
+  unit_offsets(U0, cur.pos);
+  issue(fs, cur);
+  unit_offsets(U0 + 1, offn);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) issue_x(fs, q);
+
+  for (;;) {
+    const MStep cs = fs;
+    if (!cs.valid) break;
+    if (cs.di != ddi) {
+      ddi = cs.di;
+      const auto& D = desc_at<TABLE>(a, ddi);
+      dn = D.n;
+      grouped = (D.mode & kModeGrouped) != 0;
+      raw = !BF16 && (D.mode & kModeRaw);
+      dxs = XS && (D.mode & kModeXscale);
+      scaled = !raw && (grouped || dxs);
+      tscale = half_bits_to_float(gp_u16(D.scales)[0]);
+      ry = make_rsrc(D.y, D.y_bytes);
+    }
+
+    // Word positions: popcounts exchanged among the four lanes of each row.
+    uint32_t rel[RT][4];
+    uint32_t stot[RT];
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+      uint32_t v = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v |= static_cast<uint32_t>(__builtin_popcount(cur.P[r][q])) << (8 * q);
+      const uint32_t b = static_cast<uint32_t>(__shfl_xor(static_cast<int>(v), 16, kWave));
+      const uint32_t pair = v + b;
+      const uint32_t c2 = static_cast<uint32_t>(__shfl_xor(static_cast<int>(pair), 32, kWave));
+      const uint32_t excl = ((g & 1) ? b : 0u) + ((g & 2) ? c2 : 0u);
+      const uint32_t tot = pair + c2;  // bytes <= 128
+      uint32_t cum = cur.pos[r] & 31u;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        rel[r][q] = cum + __builtin_amdgcn_ubfe(excl, 8 * q, 8);
+        cum += __builtin_amdgcn_ubfe(tot, 8 * q, 8);
+      }
+      stot[r] = cum - (cur.pos[r] & 31u);
+    }
+
+    // Fetch step t+1.
+    fs = advance(cs);
+    if (fs.c == 0) {
+#pragma unroll
+      for (int r = 0; r < RT; ++r) nxt.pos[r] = offn[r];
+      unit_offsets(fbeg + fs.unit + 1, offn);
+    } else {
+#pragma unroll
+      for (int r = 0; r < RT; ++r) nxt.pos[r] = cur.pos[r] + stot[r];
+    }
+    issue(fs, nxt);
+
+    // This step's sign dwords into the wave's LDS block.
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+      uint32_t* row = stage + (kMfmaTile * r + nr) * kSignStride;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) row[4 * g + j] = cur.SA[r][j];
+      row[16 + g] = cur.SB[r];
+    }
+    __builtin_amdgcn_wave_barrier();
+
+    // Groups: the MFMAs of group q, then the epilogue of group q - 1 (whose
+    // MFMAs have had a group's worth of work to finish).
+    CV cg[2][RT];
+    float xa_prev[4];
+    auto epilogue = [&](int q, const CV (&c)[RT], const float (&xa)[4]) {
+#pragma unroll
+      for (int r = 0; r < RT; ++r) {
+        if (scaled) {
+          const float sc = (grouped ? half_bits_to_float(static_cast<uint16_t>(cur.SC[r][q])) : tscale) *
+                           (BF16 ? 2.0f : 1.0f);
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            acc[r][i] = __builtin_fmaf(dxs ? sc * xa[i] : sc, static_cast<float>(c[r][i]), acc[r][i]);
+        } else if constexpr (BF16) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc[r][i] += static_cast<float>(c[r][i]);
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) iacc[r][i] += static_cast<int>(c[r][i]);
+        }
+      }
+    };
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+#pragma unroll
+      for (int r = 0; r < RT; ++r) {
+        const uint32_t* srow = stage + (kMfmaTile * r + nr) * kSignStride;
+        const uint32_t bpos = rel[r][q];
+        const uint32_t S = __builtin_amdgcn_alignbit(srow[(bpos >> 5) + 1], srow[bpos >> 5], bpos);
+        const uint32_t Pw = cur.P[r][q];
+        CV c = CV{0, 0, 0, 0};
+        uint32_t rr = 0;
+        if constexpr (BF16) {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const uint32_t m = __builtin_amdgcn_ubfe(Pw, 8 * j, 8);
+            const uint32_t s = __builtin_amdgcn_ubfe(S, rr, 8);
+            rr = __builtin_popcount(m) + rr;
+            const uint4 sb = tab.selb[m * NC + cp];
+            const uint2 th = tab.tsh[s * NC + cp];
+            const u32x4_t w = {__builtin_amdgcn_perm(th.y, th.x, sb.x), __builtin_amdgcn_perm(th.y, th.x, sb.y),
+                               __builtin_amdgcn_perm(th.y, th.x, sb.z), __builtin_amdgcn_perm(th.y, th.x, sb.w)};
+            c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, A[q][j]),
+                                                        __builtin_bit_cast(bf16x8_t, w), c, 0, 0, 0);
+          }
+        } else {
+          uint2 wb[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const uint32_t m = __builtin_amdgcn_ubfe(Pw, 8 * j, 8);
+            const uint32_t s = __builtin_amdgcn_ubfe(S, rr, 8);
+            rr = __builtin_popcount(m) + rr;
+            const uint2 ex = tab.exp[m * NC + cp];
+            const uint2 tg = tab.tsg[s * NC + cp];
+            wb[j] = make_uint2(__builtin_amdgcn_perm(tg.y, tg.x, ex.x), __builtin_amdgcn_perm(tg.y, tg.x, ex.y));
+          }
+#pragma unroll
+          for (int j = 0; j < 2; ++j) {
+            const u32x4_t w = {wb[2 * j].x, wb[2 * j].y, wb[2 * j + 1].x, wb[2 * j + 1].y};
+            c = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4_t, A[q][j]),
+                                                      __builtin_bit_cast(i32x4_t, w), c, 0, 0, 0);
+          }
+        }
+        cg[q & 1][r] = c;
+      }
+      // This group's activations are consumed: fetch step t+1's.
+      float xa_q[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) xa_q[i] = XS ? XA[q][i] : 1.0f;
+      issue_x(fs, q);
+      if (q > 0) epilogue(q - 1, cg[(q - 1) & 1], xa_prev);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) xa_prev[i] = xa_q[i];
+    }
+    epilogue(3, cg[1], xa_prev);
+    __builtin_amdgcn_wave_barrier();
+
+    if (cs.last) {  // store the unit: y[m][row]; rows past n and batch rows past M are dropped
+      const int row0 = cs.unit * kMfmaRows;
+#pragma unroll
+      for (int r = 0; r < RT; ++r) {
+        const int row = row0 + kMfmaTile * r + nr;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const uint32_t off = row < dn ? (static_cast<uint32_t>((4 * g + i) * dn) + row) * 4u : kOOB;
+          float f;
+          if (scaled)
+            f = acc[r][i];
+          else if constexpr (BF16)
+            f = tscale * (2.0f * acc[r][i]);
+          else
+            f = tscale * static_cast<float>(iacc[r][i]);
+          const uint32_t bits = raw ? static_cast<uint32_t>(iacc[r][i]) : __builtin_bit_cast(uint32_t, f);
+          __builtin_amdgcn_raw_buffer_store_b32(bits, ry, off, 0, 0);
+          acc[r][i] = 0.0f;
+          iacc[r][i] = 0;
+        }
+      }
+    }
+    cur = nxt;
+  }
+}
+
+using MfmaFn = void (*)(const KernelArgs);
+
+inline MfmaFn pick_mfma(bool bf16, bool xs, bool table) {
+  if (bf16) {
+    if (xs) return table ? bitcos_mfma_kernel<true, true, true> : bitcos_mfma_kernel<true, true, false>;
+    return table ? bitcos_mfma_kernel<true, false, true> : bitcos_mfma_kernel<true, false, false>;
+  }
+  if (xs) return table ? bitcos_mfma_kernel<false, true, true> : bitcos_mfma_kernel<false, true, false>;
+  return table ? bitcos_mfma_kernel<false, false, true> : bitcos_mfma_kernel<false, false, false>;
+}
+
+}  // namespace bitcos_k

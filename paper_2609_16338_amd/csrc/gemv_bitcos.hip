@@ -76,7 +76,26 @@ extern "C" int bitcos_gemv(const bitcos_layout* L, const void* blob_dev, int32_t
                            const void* x_dev, int32_t x_dtype, const float* xscale_dev,
                            void* y_dev, int32_t y_mode, void* stream) {
   if (!L || L->format != BITCOS_FMT_BITCOS) return BITCOS_E_ARG;
-  if (m != 1) return m < 1 ? BITCOS_E_ARG : BITCOS_E_UNSUPPORTED;
+  if (m < 1 || m > BITCOS_MAX_M) return BITCOS_E_ARG;
+  if (m > 1) {
+    if (!bitcos::mfma_layout_ok(L))
+      return bitcos::gemv_rows(bitcos_gemv, L, blob_dev, m, x_dev, x_dtype, xscale_dev, y_dev, y_mode, stream);
+    bitcos::GemvDesc d;
+    int st = bitcos::make_desc(L, blob_dev, x_dev, xscale_dev, y_dev, x_dtype, y_mode, &d, m);
+    if (st) return st;
+    bitcos::to_mfma_units(&d);
+    bitcos::BatchHeader h{};
+    h.magic = bitcos::kBatchMagic;
+    h.version = BITCOS_LAYOUT_VERSION;
+    h.format = BITCOS_FMT_BITCOS;
+    h.count = 1;
+    h.x_dtype = x_dtype;
+    h.y_mode = y_mode;
+    h.m = m;
+    h.any_xscale = xscale_dev != nullptr;
+    h.total_units = d.units;
+    return bitcos::launch_bitcos_mfma(h, nullptr, d, stream);
+  }
   bitcos::GemvDesc d;
   int st = bitcos::make_desc(L, blob_dev, x_dev, xscale_dev, y_dev, x_dtype, y_mode, &d);
   if (st) return st;
@@ -87,6 +106,7 @@ extern "C" int bitcos_gemv(const bitcos_layout* L, const void* blob_dev, int32_t
   h.count = 1;
   h.x_dtype = x_dtype;
   h.y_mode = y_mode;
+  h.m = 1;
   int rows = 0;
   st = bitcos::tile_for(L, x_dtype, &h.per_lane, &h.seg, &rows);
   if (st) return st;

@@ -40,7 +40,10 @@ static int fixed_gemv(uint32_t fmt, const bitcos_layout* L, const void* blob_dev
                       const void* x_dev, int32_t x_dtype, const float* xscale_dev, void* y_dev,
                       int32_t y_mode, void* stream) {
   if (!L || L->format != fmt) return BITCOS_E_ARG;
-  if (m != 1) return m < 1 ? BITCOS_E_ARG : BITCOS_E_UNSUPPORTED;
+  if (m < 1 || m > BITCOS_MAX_M) return BITCOS_E_ARG;
+  if (m > 1)
+    return bitcos::gemv_rows(fmt == BITCOS_FMT_TRIT5 ? trit5_gemv : bit2_gemv, L, blob_dev, m, x_dev, x_dtype,
+                             xscale_dev, y_dev, y_mode, stream);
   bitcos::GemvDesc d;
   int st = bitcos::make_desc(L, blob_dev, x_dev, xscale_dev, y_dev, x_dtype, y_mode, &d);
   if (st) return st;
@@ -51,6 +54,7 @@ static int fixed_gemv(uint32_t fmt, const bitcos_layout* L, const void* blob_dev
   h.count = 1;
   h.x_dtype = x_dtype;
   h.y_mode = y_mode;
+  h.m = 1;
   int rows = 0;
   st = bitcos::tile_for(L, x_dtype, &h.per_lane, &h.seg, &rows);
   if (st) return st;

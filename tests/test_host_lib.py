@@ -185,12 +185,30 @@ def test_gemv_validation_happens_before_any_device_work():
     g = N.lib().bitcos_gemv
     assert g(ctypes.byref(L), None, 1, dummy, N.X_I8, None, dummy, N.Y_F32, None) == N.E_ARG
     assert g(ctypes.byref(L), dummy, 0, dummy, N.X_I8, None, dummy, N.Y_F32, None) == N.E_ARG
-    assert g(ctypes.byref(L), dummy, 17, dummy, N.X_I8, None, dummy, N.Y_F32, None) == N.E_UNSUPPORTED
+    assert g(ctypes.byref(L), dummy, 17, dummy, N.X_I8, None, dummy, N.Y_F32, None) == N.E_ARG
+    assert g(ctypes.byref(L), dummy, 4, dummy, 7, None, dummy, N.Y_F32, None) == N.E_ARG
+    assert g(ctypes.byref(L), dummy, 16, dummy, N.X_BF16, None, dummy, N.Y_I32_RAW, None) == N.E_ARG
+    assert g(ctypes.byref(L), None, 2, dummy, N.X_I8, None, dummy, N.Y_F32, None) == N.E_ARG
+    L4 = api.bitcos_plan(w, 128, 4)   # four rows per sign offset: m batch-1 launches, same checks first
+    assert g(ctypes.byref(L4), dummy, 3, dummy, 7, None, dummy, N.Y_F32, None) == N.E_ARG
     assert g(ctypes.byref(L), dummy, 1, dummy, 7, None, dummy, N.Y_F32, None) == N.E_ARG
     assert g(ctypes.byref(L), dummy, 1, dummy, N.X_BF16, None, dummy, N.Y_I32_RAW, None) == N.E_ARG
     Lt = api.trit5_plan(w, 128)
     assert N.lib().trit5_gemv(ctypes.byref(L), dummy, 1, dummy, N.X_I8, None, dummy, N.Y_F32, None) == N.E_ARG
     assert N.lib().bit2_gemv(ctypes.byref(Lt), dummy, 1, dummy, N.X_I8, None, dummy, N.Y_F32, None) == N.E_ARG
+    assert N.lib().trit5_gemv(ctypes.byref(Lt), dummy, 17, dummy, N.X_I8, None, dummy, N.Y_F32, None) == N.E_ARG
+    assert N.lib().trit5_gemv(ctypes.byref(Lt), dummy, 5, dummy, 9, None, dummy, N.Y_F32, None) == N.E_ARG
+
+
+def test_describe_small_batch():
+    w = np.zeros((100, 2560), np.int8)
+    L = api.bitcos_plan(w, 128, 0)
+    info = api.describe(L, 16, N.X_BF16)
+    assert (info.seg_lanes, info.rows_per_step, info.per_lane) == (4, 32, 1)
+    assert info.waves == 4                      # ceil(100 / 32) units of 32 rows
+    with pytest.raises(N.BitcosError) as e:
+        api.describe(L, 17, N.X_I8)
+    assert e.value.status == N.E_ARG
 
 
 def test_describe_tiles():
