@@ -61,7 +61,9 @@ struct BatchHeader {
   int32_t unit_is_step;  // every GEMV's unit is one wave step (BITCOS streaming kernel)
   int32_t m;             // activation rows (> 1: the small-batch MFMA kernel)
   int32_t any_xscale;    // some GEMV has activation scales
-  int32_t reserved[19];
+  int32_t any_grouped;   // some GEMV has group scales
+  int32_t row_offsets;   // every BITCOS GEMV stores one sign offset per row
+  int32_t reserved[17];
 };
 static_assert(sizeof(BatchHeader) == 128, "BatchHeader is 128 bytes");
 

@@ -171,6 +171,7 @@ int bitcos_batch_build(int32_t count, int32_t m, const bitcos_layout* layouts, c
   int64_t units = 0;
   int step_rows = 0;
   h.unit_is_step = 1;
+  h.row_offsets = 1;
   for (int32_t i = 0; i < count; ++i) {
     const bitcos_layout* L = &layouts[i];
     if (L->format != h.format) return BITCOS_E_UNSUPPORTED;
@@ -186,6 +187,9 @@ int bitcos_batch_build(int32_t count, int32_t m, const bitcos_layout* layouts, c
     st = bitcos::make_desc(L, blobs_dev[i], x_dev[i], xscale_dev ? xscale_dev[i] : nullptr, y_dev[i],
                            x_dtype, y_mode, &descs[i]);
     if (st) return st;
+    if (descs[i].mode & bitcos::kModeXscale) h.any_xscale = 1;
+    if (descs[i].mode & bitcos::kModeGrouped) h.any_grouped = 1;
+    if (descs[i].unit_rows != 1) h.row_offsets = 0;
     if (h.format != BITCOS_FMT_BITCOS || rows % descs[i].unit_rows) h.unit_is_step = 0;
     step_rows = rows;
   }

@@ -1,0 +1,8 @@
+// BITCOS batch-1 kernels with the multiply on the matrix cores, 32 lanes per
+// row segment (one file per segment width so the instantiations compile in
+// parallel).
+#include "bitcos_diag.h"
+
+namespace bitcos_k {
+FastFn pick_diag_seg_32(int per_lane, bool bf16, bool table) { return pick_diag_seg<32>(per_lane, bf16, table); }
+}  // namespace bitcos_k
