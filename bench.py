@@ -64,7 +64,7 @@ def parse():
 # reported only while these files are unchanged.
 KERNEL_SOURCES = ["bitcos_diag.h", "bitcos_fast.h", "bitcos_kernel.h", "mfma_common.h", "device_common.h", "batch.h",
                   "batch.hip", "gemv_bitcos.hip", "gemv_bitcos_d16.hip", "launch_common.h", "plan.h"]
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "bitcos_fast_bf16_bitnet2b_k2560_traffic.txt")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "bitcos_diag_bf16_bitnet2b_k2560_traffic.txt")
 COPY_MIB = 256
 
 
@@ -501,15 +501,10 @@ def main():
         "speedup_vs_trit5": round(res[(N.FMT_TRIT5, "int8")] / ms8, 4) if N.FMT_TRIT5 in fmts else None,
         "speedup_vs_bit2": round(res[(N.FMT_BIT2, "int8")] / ms8, 4) if N.FMT_TRIT5 in fmts else None,
     }
-    # Which kernel the launcher picks for this batch: the matrix-core one for
-    # one scale per tensor and no activation scales (and one sign offset per
-    # row at 16 or fewer lanes per row), else the streaming one, else the
-    # general one.
-    info = api.describe(top.entries[0][3], 1, N.X_BF16)
-    streaming = all(info.rows_per_step % e[3].unit_rows == 0 for e in top.entries)
-    diag = streaming and all(e[3].group == 0 for e in top.entries) and (
-        info.seg_lanes > 16 or all(e[3].unit_rows == 1 for e in top.entries))
-    kname = "bitcos_diag_kernel" if diag else "bitcos_fast_kernel" if streaming else "bitcos_gemv_kernel"
+    # The kernel the launcher picks (all GEMVs of the launch share layout kind and tile).
+    kinds = {api.describe(e[3], 1, N.X_BF16).kernel for e in top.entries}
+    kname = {N.KERNEL_MATRIX: "bitcos_diag_kernel", N.KERNEL_STREAMING: "bitcos_fast_kernel",
+             N.KERNEL_GENERAL: "bitcos_gemv_kernel"}.get(kinds.pop(), "?") if len(kinds) == 1 else "mixed"
     out["roofline"] = {
         "bound": "hbm",
         "achieved": round(achieved, 2),

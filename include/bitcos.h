@@ -257,9 +257,16 @@ int bitcos_pack_device(const int8_t* w_dev, const uint16_t* scales_dev, const bi
                        void* ws_dev, size_t ws_bytes, void* dst_dev, size_t cap, void* stream);
 
 /* ---- launch description (for measurement) ---------------------------------
- * Fills the kernel configuration a GEMV on this layout would launch with:
- * words (or blocks) per lane, lanes per row segment, rows per wave step,
- * waves and workgroups.  Errors as for the GEMV. */
+ * Fills the kernel configuration a GEMV on this layout would launch with,
+ * for a call (or a batch of such layouts) without activation scales: words
+ * (or blocks) per lane, lanes per row segment, rows per wave step, waves and
+ * workgroups, and which kernel runs (BITCOS_KERNEL_*).  Errors as for the
+ * GEMV. */
+#define BITCOS_KERNEL_GENERAL 1     /* BITCOS, any rows per sign offset                          */
+#define BITCOS_KERNEL_STREAMING 2   /* BITCOS batch 1, group scales: v_dot2 / v_dot4 multiply    */
+#define BITCOS_KERNEL_MATRIX 3      /* BITCOS batch 1, one scale per tensor: multiply on MFMA    */
+#define BITCOS_KERNEL_SMALL_BATCH 4 /* BITCOS, 2..16 activation rows on MFMA                     */
+#define BITCOS_KERNEL_FIXED 5       /* five-trit or 2-bit                                        */
 typedef struct bitcos_launch_info {
   int32_t per_lane;        /* BITCOS: 32-weight words per lane; TRIT5: 128-blocks; BIT2: 16-weight words */
   int32_t seg_lanes;       /* lanes that share one row (power of two)          */
@@ -267,6 +274,8 @@ typedef struct bitcos_launch_info {
   int32_t lanes_used;      /* lanes per row that hold weights                   */
   int64_t waves;           /* waves launched                                   */
   int64_t workgroups;      /* workgroups launched (256 threads each)           */
+  int32_t kernel;          /* BITCOS_KERNEL_*                                   */
+  int32_t reserved;
 } bitcos_launch_info;
 
 int bitcos_describe(const bitcos_layout* L, int32_t m, int32_t x_dtype, bitcos_launch_info* out);

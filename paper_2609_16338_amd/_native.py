@@ -25,6 +25,7 @@ SEC_CODES = 0
 X_I8, X_BF16 = 1, 2
 Y_F32, Y_I32_RAW = 1, 2
 MAX_M = 16  # most activation rows per GEMV call
+KERNEL_GENERAL, KERNEL_STREAMING, KERNEL_MATRIX, KERNEL_SMALL_BATCH, KERNEL_FIXED = 1, 2, 3, 4, 5
 LAYOUT_VERSION = 1
 
 
@@ -57,6 +58,8 @@ class LaunchInfo(ctypes.Structure):
         ("lanes_used", ctypes.c_int32),
         ("waves", ctypes.c_int64),
         ("workgroups", ctypes.c_int64),
+        ("kernel", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
     ]
 
 

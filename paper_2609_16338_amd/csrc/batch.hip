@@ -219,6 +219,8 @@ int bitcos_gemv_batch(const void* table_host, const void* table_dev, void* strea
   return bitcos::launch(h, descs, *first, stream);
 }
 
+static_assert(sizeof(bitcos_launch_info) == 40, "bitcos_launch_info is 40 bytes (the Python binding mirrors it)");
+
 int bitcos_describe(const bitcos_layout* L, int32_t m, int32_t x_dtype, bitcos_launch_info* out) {
   if (!L || !out) return BITCOS_E_ARG;
   if (m < 1 || m > BITCOS_MAX_M) return BITCOS_E_ARG;
@@ -233,6 +235,8 @@ int bitcos_describe(const bitcos_layout* L, int32_t m, int32_t x_dtype, bitcos_l
     out->lanes_used = 4;
     out->waves = units;
     out->workgroups = (units + 7) / 8;
+    out->kernel = BITCOS_KERNEL_SMALL_BATCH;
+    out->reserved = 0;
     return BITCOS_OK;
   }
   int per_lane = 0, seg = 0, rows = 0;
@@ -247,6 +251,14 @@ int bitcos_describe(const bitcos_layout* L, int32_t m, int32_t x_dtype, bitcos_l
   out->lanes_used = (upr + per_lane - 1) / per_lane;
   out->waves = units;          // upper bound: persistent grids use at most the resident waves
   out->workgroups = (units + 3) / 4;
+  out->reserved = 0;
+  if (L->format != BITCOS_FMT_BITCOS) {
+    out->kernel = BITCOS_KERNEL_FIXED;
+  } else {  // the choice launch_bitcos makes (batch 1; m > 1 here runs m batch-1 calls)
+    const bool streaming = rows % L->unit_rows == 0 && (L->n + rows - 1) / rows < (int64_t(1) << 30);
+    const bool matrix = streaming && L->group == 0 && (seg > 16 || L->unit_rows == 1);
+    out->kernel = matrix ? BITCOS_KERNEL_MATRIX : streaming ? BITCOS_KERNEL_STREAMING : BITCOS_KERNEL_GENERAL;
+  }
   return BITCOS_OK;
 }
 

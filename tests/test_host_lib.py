@@ -49,7 +49,7 @@ def test_version_and_strerror():
 
 def test_layout_struct_size():
     assert ctypes.sizeof(N.Layout) == 112
-    assert ctypes.sizeof(N.LaunchInfo) == 32
+    assert ctypes.sizeof(N.LaunchInfo) == 40
 
 
 ENC = {N.FMT_BITCOS: O.bitcos_encode, N.FMT_TRIT5: O.trit5_encode, N.FMT_BIT2: O.bit2_encode}
@@ -219,3 +219,32 @@ def test_describe_tiles():
         assert (info.per_lane, info.seg_lanes) == (per_lane, seg), k
         assert info.rows_per_step * info.seg_lanes == 64
         assert info.lanes_used * info.per_lane >= k // 32
+
+
+def test_describe_kernel_choice():
+    """Which kernel a batch-1 call on a layout runs (the launcher's rule)."""
+    def kind(group, unit_rows, k=2560, fmt=N.FMT_BITCOS, m=1, x=N.X_BF16):
+        w = np.zeros((40, k), np.int8)
+        if fmt == N.FMT_BITCOS:
+            L = api.bitcos_plan(w, group, unit_rows)
+        elif fmt == N.FMT_TRIT5:
+            L = api.trit5_plan(w, group)
+        else:
+            L = api.bit2_plan(w, group)
+        return api.describe(L, m, x).kernel
+    # one scale per tensor, one offset per row: matrix cores (either activation type)
+    assert kind(0, 1) == N.KERNEL_MATRIX
+    assert kind(0, 1, x=N.X_I8) == N.KERNEL_MATRIX
+    # group scales: the streaming kernel
+    assert kind(128, 1) == N.KERNEL_STREAMING
+    # several rows per offset at 16 lanes per row (K = 2560): the prefix needs per-row offsets
+    assert kind(0, 2) == N.KERNEL_STREAMING
+    # ... but not at 32 or more lanes per row (K = 6912: 32 lanes, 2 rows per step)
+    assert kind(0, 2, k=6912) == N.KERNEL_MATRIX
+    # a unit that does not divide the wave step: the general kernel
+    assert kind(0, 3) == N.KERNEL_GENERAL
+    assert kind(128, 3) == N.KERNEL_GENERAL
+    # small batch and the baselines
+    assert kind(0, 1, m=4) == N.KERNEL_SMALL_BATCH
+    assert kind(0, 0, fmt=N.FMT_TRIT5) == N.KERNEL_FIXED
+    assert kind(128, 0, fmt=N.FMT_BIT2) == N.KERNEL_FIXED
