@@ -298,11 +298,10 @@ __global__ void __launch_bounds__(diag_threads(W, BF16)) bitcos_diag_kernel(cons
   // Sign buffer of one wave and stage: the largest step block (64 lanes x W
   // words, all non-zero) plus the dword a window reads past its start and
   // the step's in-dword offset, rounded to 16 bytes.  It is filled in
-  // 1 KB chunks (16 bytes per lane); the last chunk's lanes past the buffer
-  // are masked off.
+  // 1 KB chunks (16 bytes per lane), of which only the lanes inside the
+  // step's block load.
   constexpr int SCR = diag_sign_dwords(W);
   constexpr int NSC = (SCR + 255) / 256;
-  constexpr int LAST_LANES = (SCR - 256 * (NSC - 1)) / 4;
   using Acc = typename std::conditional<BF16, float, int>::type;
   using CV = typename std::conditional<BF16, f32x4_t, i32x4_t>::type;
 
@@ -386,21 +385,38 @@ __global__ void __launch_bounds__(diag_threads(W, BF16)) bitcos_diag_kernel(cons
     if (s.valid && s.di != idi) fetch_enter(s.di);
     const uint32_t unit = static_cast<uint32_t>(s.row0 / R);
     const uint32_t soff_p = __builtin_amdgcn_readfirstlane(s.valid ? unit * row_bytes : kOOB);
+    // The lane's words: the first four in one 16-byte load (dword-aligned;
+    // dwords past the section read zero), the rest one by one.
+    if constexpr (W >= 4) {
+      const u32x4_t v = ld128_s(rb, voff_p, soff_p);
 #pragma unroll
-    for (int w = 0; w < W; ++w) P[k][w] = __builtin_amdgcn_raw_buffer_load_b32(rb, voff_p + 4u * w, soff_p, 0);
+      for (int w = 0; w < 4; ++w) P[k][w] = v[w];
+#pragma unroll
+      for (int w = 4; w < W; ++w) P[k][w] = __builtin_amdgcn_raw_buffer_load_b32(rb, voff_p + 4u * w, soff_p, 0);
+    } else {
+#pragma unroll
+      for (int w = 0; w < W; ++w) P[k][w] = __builtin_amdgcn_raw_buffer_load_b32(rb, voff_p + 4u * w, soff_p, 0);
+    }
     if constexpr (kRowOffsets) {  // rows past the matrix end read the last entry (nnz)
       const int e = min(static_cast<int>(unit) * gen.stride + rho, gen.last);
       ROFF[k] = ld32(ro, s.valid ? static_cast<uint32_t>(e) * 4u : kOOB);
     }
+    // The step's sign block: dwords [off0 / 32, off1 / 32 + 1] are the most
+    // any window reads.  Only the 16-byte pieces of that range are fetched
+    // (lane l of chunk c lands at byte 1024 c + 16 l of the wave's buffer);
+    // LDS past it keeps stale bits no window uses.
     const uint32_t d0 = s.off0 >> 5;
-    const uint32_t need = ((s.off1 >> 5) + 2u - d0) * 4u;
+    const int pieces = static_cast<int>((((s.off1 >> 5) + 2u - d0) * 4u + 15u) >> 4);
     uint4* dst = stage_buf(stage_c) + wv * (SCR / 4);
 #pragma unroll
     for (int c = 0; c < NSC; ++c) {
-      const uint32_t soff_s = __builtin_amdgcn_readfirstlane((s.valid && 1024u * c < need) ? d0 * 4u + 1024u * c : kOOB);
-      if (c + 1 < NSC || lane < LAST_LANES)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rg, (__attribute__((address_space(3))) void*)(dst + 64 * c), 16,
-                                                 voff_s, soff_s, 0, 0);
+      const int lanes_c = __builtin_amdgcn_readfirstlane(pieces - 64 * c);
+      if (s.valid && lanes_c > 0) {
+        const uint32_t soff_s = __builtin_amdgcn_readfirstlane(d0 * 4u + 1024u * c);
+        if (lane < lanes_c)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rg, (__attribute__((address_space(3))) void*)(dst + 64 * c), 16,
+                                                   voff_s, soff_s, 0, 0);
+      }
     }
   };
 
@@ -463,13 +479,16 @@ __global__ void __launch_bounds__(diag_threads(W, BF16)) bitcos_diag_kernel(cons
     }
     __builtin_amdgcn_wave_barrier();
 
-    // Windows: 64 bits at each word's first sign, clamped to the wave's own
-    // buffer (a valid cursor never needs the clamp).
+    // Windows: 64 bits at each word's first sign.  The lane's cursor is
+    // clamped once so that every window stays in the wave's own buffer (a
+    // valid cursor never needs it; a word's offset in the lane is < 32 W).
     uint32_t S[W];
+    const uint32_t bclamp = min(base, wave_bits + (SCR - 2 - W) * 32u);
 #pragma unroll
     for (int w = 0; w < W; ++w) {
-      const uint32_t b = min(base + static_cast<uint32_t>(pc[w]), wave_bits + (SCR - 2) * 32u);
-      S[w] = __builtin_amdgcn_alignbit(scr32[(b >> 5) + 1], scr32[b >> 5], b);
+      const uint32_t b = bclamp + static_cast<uint32_t>(pc[w]);
+      const uint32_t* sp = scr32 + (b >> 5);
+      S[w] = __builtin_amdgcn_alignbit(sp[1], sp[0], b);
     }
     // Two accumulators, alternating, so consecutive MFMAs do not wait on each
     // other; word w + 1's lookups are in flight while word w is multiplied

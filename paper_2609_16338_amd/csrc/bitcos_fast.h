@@ -204,18 +204,22 @@ __global__ void __launch_bounds__(fast_threads(W, BF16)) bitcos_fast_kernel(cons
 #pragma unroll
     for (int w = 0; w < W; ++w) P[k][w] = __builtin_amdgcn_raw_buffer_load_b32(rb, voff_p + 4u * w, soff_p, 0);
     // The step's sign block: dwords [off0 / 32, off1 / 32 + 1] are the most
-    // any window reads; chunks past that are not fetched.
+    // any window reads.  Only the 16-byte pieces of that range are fetched,
+    // straight into this wave's part of the stage buffer (lane l of chunk c
+    // lands at byte 1024 c + 16 l); LDS past it keeps stale bits no window
+    // uses.
     const uint32_t d0 = s.off0 >> 5;
-    const uint32_t need = ((s.off1 >> 5) + 2u - d0) * 4u;
-    // Straight into this wave's part of the stage buffer: lane l's 16 bytes
-    // of chunk c land at byte 1024 c + 16 l.  Chunks past the step's range
-    // read zero.
+    const int pieces = static_cast<int>((((s.off1 >> 5) + 2u - d0) * 4u + 15u) >> 4);
     uint4* dst = stage_buf(stage_c) + wv * (SCR / 4);
 #pragma unroll
     for (int c = 0; c < NSC; ++c) {
-      const uint32_t soff_s = __builtin_amdgcn_readfirstlane((s.valid && 1024u * c < need) ? d0 * 4u + 1024u * c : kOOB);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rg, (__attribute__((address_space(3))) void*)(dst + 64 * c), 16, voff_s,
-                                               soff_s, 0, 0);
+      const int lanes_c = __builtin_amdgcn_readfirstlane(pieces - 64 * c);
+      if (s.valid && lanes_c > 0) {
+        const uint32_t soff_s = __builtin_amdgcn_readfirstlane(d0 * 4u + 1024u * c);
+        if (lane < lanes_c)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rg, (__attribute__((address_space(3))) void*)(dst + 64 * c), 16,
+                                                   voff_s, soff_s, 0, 0);
+      }
     }
     const uint32_t soff_q = __builtin_amdgcn_readfirstlane((s.valid && grouped) ? unit * row_scale_bytes : kOOB);
 #pragma unroll

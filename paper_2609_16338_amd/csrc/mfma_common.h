@@ -52,5 +52,8 @@ __device__ __forceinline__ void build_mfma_tables(Tables<true>& t, int tid, int 
 __device__ __forceinline__ u32x4_t ld128(rsrc_t r, uint32_t off) {
   return __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
 }
+__device__ __forceinline__ u32x4_t ld128_s(rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
 
 }  // namespace bitcos_k
