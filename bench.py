@@ -2,7 +2,9 @@
 """Benchmark: BITCOS ternary GEMV effective weight bandwidth on one MI355X.
 
 A step is one batch-1 pass over a whole decode layer set (every GEMV of every
-layer, inputs already resident in HBM), replayed from a HIP graph.  The
+layer, inputs already resident in HBM), replayed from a HIP graph: W untimed
+replays, then K timed ones, after a one-off 100 ms untimed warm-up that lifts
+the GPU out of the idle clocks of the host-side packing.  The
 headline is the BitNet-2B-like set: 30 layers x {q, o 2560x2560; k, v
 640x2560; gate, up 6912x2560; down 2560x6912}, z = 0.42 iid, one fp16 scale
 per tensor, bf16 activations ~ N(0, 1) (the int8-quantised variant is reported
@@ -11,7 +13,8 @@ step time.  The same step over the five-trit and 2-bit layouts of the same
 weights gives the same-GPU speedups.
 
 Prints ONE JSON line.  roofline: the dominant launch (the K = 2560 GEMVs of
-the step, one persistent launch) timed alone from a graph; achieved = its
+the step, one persistent launch) timed alone, from a graph of ten back-to-back
+launches; achieved = its
 algorithmic bytes (payload + 2 K activation bytes + 4 N output bytes per GEMV)
 per launch time, against the 8 TB/s HBM peak; traffic = its measured HBM
 bytes (FETCH_SIZE + WRITE_SIZE scaled by a plain copy's counters, stored under
@@ -42,8 +45,8 @@ METRIC = "ternary GEMV effective weight GB/s (% of 8 TB/s HBM peak); speedup vs 
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--workload", default="bitnet2b_layers")
     ap.add_argument("--layers", type=int, default=0, help="0 = the workload's layer count")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -204,6 +207,24 @@ def time_graph(g, steps, warmup):
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     return start.elapsed_time(end) / steps, wall
+
+
+def warm_device(g, min_ms=100.0):
+    """Replay a graph for at least `min_ms` of wall time, untimed.
+
+    After the host-side packing the GPU has idled and its clocks start low:
+    the first ~150 replays of the BitNet-like step run up to 20% slower than
+    the steady state a decode loop sees.  This brings the device to that
+    state once, before anything is timed."""
+    import torch
+    t0 = time.perf_counter()
+    n = 0
+    while (time.perf_counter() - t0) * 1e3 < min_ms:
+        for _ in range(20):
+            g.replay()
+        n += 20
+        torch.cuda.synchronize()
+    return n, (time.perf_counter() - t0) * 1e3
 
 
 def cpu_baseline(wk, budget_s=12.0):
@@ -438,6 +459,9 @@ def main():
         for kind in ("bf16", "int8"):
             step, _ = make_step(packed[fmt], acts, kind)
             g = capture(step)
+            if not res:
+                n, wms = warm_device(g)
+                print(f"[bench] device warm-up: {n} untimed replays in {wms:.0f} ms", file=sys.stderr, flush=True)
             ms, wall = time_graph(g, args.steps, args.warmup)
             res[(fmt, kind)] = ms
             print(f"[bench] fmt={fmt} {kind}: {ms * 1e3:.1f} us/step, "
@@ -446,12 +470,16 @@ def main():
 
     # Dominant kernel: the batched BITCOS launch carrying most of the bytes
     # (the K = 2560 tile for this set: q, k, v, o, gate, up of every layer),
-    # timed alone from a graph of that one launch.
+    # timed alone.
     batches = make_batches(packed[N.FMT_BITCOS], acts, "bf16")
     top = batches[0]
-    gg = capture(top.run)
+    # Ten back-to-back launches per replay: inside a graph consecutive
+    # kernels start without a gap, so replay overhead stays out of the
+    # per-launch time.
+    reps = 10
+    gg = capture(lambda: [top.run() for _ in range(reps)])
     ms_g, _ = time_graph(gg, args.steps, args.warmup)
-    per_launch_us = ms_g * 1e3
+    per_launch_us = ms_g * 1e3 / reps
     alg_bytes = sum(e[3].payload_bits / 8 + e[3].k * 2 + e[3].n * 4 for e in top.entries)
     achieved = alg_bytes / (per_launch_us * 1e-6) / 1e9
     ms = res[(N.FMT_BITCOS, "bf16")]
