@@ -429,9 +429,30 @@ __global__ void __launch_bounds__(diag_threads(W, BF16)) bitcos_diag_kernel(cons
   int nwl = W;
   rsrc_t ry = make_rsrc(nullptr, 0);
 
-  auto decode = [&](auto stage_c) {
+  // A step's output store is issued at the start of the next step, after
+  // its wait (so that wait never waits on the store).
+  bool pend = false;
+  uint32_t pend_bits = 0, pend_voff = 0, pend_soff = kOOB;
+  rsrc_t pend_ry = ry;
+  auto flush_store = [&] {
+    if (pend) __builtin_amdgcn_raw_buffer_store_b32(pend_bits, pend_ry, pend_voff, pend_soff, 0);
+    pend = false;
+  };
+
+  // Decode of one step; `next` issues the following step's loads right after
+  // this step's wait.  The step's loads (presence words, row offsets and the
+  // sign block staged into LDS) are waited for all at once: a sign block's
+  // LDS-DMA may complete after vector-memory loads issued behind it, so a
+  // counted vmcnt wait does not cover it.  With the next step's loads issued
+  // only after this wait, only this step's loads are outstanding here,
+  // issued a whole step earlier; the next step's sign block goes to the
+  // other stage buffer.
+  auto decode = [&](auto stage_c, auto&& next) {
     constexpr int k = decltype(stage_c)::value;
     const FastStep& s = st[k];
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    flush_store();
+    next();
     if (s.di != xdi) {
       xdi = s.di;
       const auto& g = desc_at<TABLE>(a, xdi);
@@ -522,8 +543,11 @@ __global__ void __launch_bounds__(diag_threads(W, BF16)) bitcos_diag_kernel(cons
       bits = __builtin_bit_cast(uint32_t, tensor_scale * static_cast<float>(tot));
     }
     // Rows past the end of the matrix fall outside ry and are dropped.
-    const uint32_t soff_y = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(s.row0) * 4u);
-    if (store) __builtin_amdgcn_raw_buffer_store_b32(bits, ry, 4u * static_cast<uint32_t>(row), soff_y, 0);
+    pend = store;
+    pend_bits = bits;
+    pend_voff = 4u * static_cast<uint32_t>(row);
+    pend_soff = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(s.row0) * 4u);
+    pend_ry = ry;
   };
 
   [&]<int... Ks>(std::integer_sequence<int, Ks...>) {
@@ -535,18 +559,20 @@ __global__ void __launch_bounds__(diag_threads(W, BF16)) bitcos_diag_kernel(cons
     [&]<int... Ks>(std::integer_sequence<int, Ks...>) {
       (([&] {
          if (!more) return;
-         constexpr int nk = (Ks + D - 1) % D;
-         st[nk] = gen.next(a);
-         issue(std::integral_constant<int, nk>{});
          if (!st[Ks].valid) {
            more = false;
            return;
          }
-         decode(std::integral_constant<int, Ks>{});
+         constexpr int nk = (Ks + D - 1) % D;
+         decode(std::integral_constant<int, Ks>{}, [&] {
+           st[nk] = gen.next(a);
+           issue(std::integral_constant<int, nk>{});
+         });
        }()),
        ...);
     }(std::make_integer_sequence<int, D>{});
   }
+  flush_store();
 }
 
 template <int SEG, bool BF16, bool TABLE, int... Ws>

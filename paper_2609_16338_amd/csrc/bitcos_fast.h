@@ -237,9 +237,30 @@ __global__ void __launch_bounds__(fast_threads(W, BF16)) bitcos_fast_kernel(cons
   rsrc_t ry = make_rsrc(nullptr, 0);
   const uint32_t voff_y = 4u * static_cast<uint32_t>(rho);
 
-  auto decode = [&](auto stage_c) {
+  // A step's output store is issued at the start of the next step, after
+  // its wait (so that wait never waits on the store).
+  bool pend = false;
+  uint32_t pend_bits = 0, pend_soff = kOOB;
+  rsrc_t pend_ry = ry;
+  auto flush_store = [&] {
+    if (pend) __builtin_amdgcn_raw_buffer_store_b32(pend_bits, pend_ry, voff_y, pend_soff, 0);
+    pend = false;
+  };
+
+  // Decode of one step; `next` issues the following step's loads right after
+  // this step's wait.  The step's loads (presence words, scales
+  // and the sign block staged into LDS) are waited for all at once: a sign
+  // block's LDS-DMA may complete after vector-memory loads issued behind it,
+  // so a counted vmcnt wait does not cover it.  With the next step's loads
+  // issued only after this wait, only this step's loads are outstanding
+  // here, issued a whole step earlier; the next step's sign block goes to
+  // the other stage buffer.
+  auto decode = [&](auto stage_c, auto&& next) {
     constexpr int k = decltype(stage_c)::value;
     const FastStep& s = st[k];
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    flush_store();
+    next();
     if (s.di != xdi) {  // entering another GEMV: its activations and scales
       xdi = s.di;
       const auto& g = desc_at<TABLE>(a, xdi);
@@ -327,7 +348,10 @@ __global__ void __launch_bounds__(fast_threads(W, BF16)) bitcos_fast_kernel(cons
     const uint32_t soff_y = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(s.row0) * 4u);
     if (!BF16 && (mode & kModeRaw)) {
       const int tot = seg_sum<SEG>(static_cast<int>(run[W - 1]));
-      if (j == SEG - 1) __builtin_amdgcn_raw_buffer_store_b32(static_cast<uint32_t>(tot), ry, voff_y, soff_y, 0);
+      pend = j == SEG - 1;
+      pend_bits = static_cast<uint32_t>(tot);
+      pend_soff = soff_y;
+      pend_ry = ry;
       return;
     }
     float part;
@@ -350,7 +374,10 @@ __global__ void __launch_bounds__(fast_threads(W, BF16)) bitcos_fast_kernel(cons
       }
       part = seg_sum<SEG>(BF16 ? 2.0f * f : f);
     }
-    if (j == SEG - 1) __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, part), ry, voff_y, soff_y, 0);
+    pend = j == SEG - 1;
+    pend_bits = __builtin_bit_cast(uint32_t, part);
+    pend_soff = soff_y;
+    pend_ry = ry;
   };
 
   // Prologue: steps 0 .. D-2 in flight.
@@ -361,21 +388,23 @@ __global__ void __launch_bounds__(fast_threads(W, BF16)) bitcos_fast_kernel(cons
   bool more = true;
   while (more) {
     [&]<int... Ks>(std::integer_sequence<int, Ks...>) {
-      // Stage Ks decodes; stage (Ks + D - 1) % D is refilled first.
+      // Stage Ks decodes; stage (Ks + D - 1) % D is refilled after its wait.
       (([&] {
          if (!more) return;
-         constexpr int nk = (Ks + D - 1) % D;
-         st[nk] = gen.next(a);
-         issue(std::integral_constant<int, nk>{});
          if (!st[Ks].valid) {
            more = false;
            return;
          }
-         decode(std::integral_constant<int, Ks>{});
+         constexpr int nk = (Ks + D - 1) % D;
+         decode(std::integral_constant<int, Ks>{}, [&] {
+           st[nk] = gen.next(a);
+           issue(std::integral_constant<int, nk>{});
+         });
        }()),
        ...);
     }(std::make_integer_sequence<int, D>{});
   }
+  flush_store();
 }
 
 using FastFn = void (*)(const KernelArgs);
