@@ -146,7 +146,10 @@ int bitcos_unpack(const bitcos_layout* L, const void* blob, size_t blob_bytes, i
  *             decode.  2 <= m <= 16 runs the small-batch kernel (every
  *             decoded weight multiplied against all m rows on the matrix
  *             cores) when the layout has one sign offset per row and
- *             k % 128 == 0; other layouts run m batch-1 launches.
+ *             k % 128 == 0; other layouts run m batch-1 launches.  At m = 1
+ *             rows longer than the batch-1 kernels take (bf16 k > 16384,
+ *             int8 k > 32768) run the small-batch kernel too, with such
+ *             layouts; others return E_UNSUPPORTED.
  *   x_dev     device activations [m][k]: int8 (BITCOS_X_I8) or bf16 bits
  *             (BITCOS_X_BF16), row-major.
  *   xscale_dev  NULL (a = 1) or device fp32 [m][k/128] per-group activation
@@ -201,8 +204,10 @@ int bit2_gemv(const bitcos_layout* L, const void* blob_dev, int32_t m, const voi
  * ([m][k/128]; entries may be NULL).  The table records the device pointers:
  * they must stay valid while the table is in use.  m > 1 takes BITCOS
  * layouts with one sign offset per row and k % 128 == 0 (the small-batch
- * kernel).  Errors: E_ARG, E_SPACE, E_UNSUPPORTED (mixed formats or tiles:
- * build one batch per tile; m > 1 with another layout).
+ * kernel); so does m = 1 when layouts[0]'s rows are longer than the batch-1
+ * tiles (bitcos_describe reports BITCOS_KERNEL_SMALL_BATCH).  Errors: E_ARG,
+ * E_SPACE, E_UNSUPPORTED (mixed formats or tiles: build one batch per tile;
+ * a small-batch table with another layout).
  *
  * bitcos_gemv_batch: copy of the table in device memory (16-byte aligned,
  * unchanged since built) plus the host table it was copied from; enqueues
@@ -265,7 +270,8 @@ int bitcos_pack_device(const int8_t* w_dev, const uint16_t* scales_dev, const bi
 #define BITCOS_KERNEL_GENERAL 1     /* BITCOS, any rows per sign offset                          */
 #define BITCOS_KERNEL_STREAMING 2   /* BITCOS batch 1, group scales: v_dot2 / v_dot4 multiply    */
 #define BITCOS_KERNEL_MATRIX 3      /* BITCOS batch 1, one scale per tensor: multiply on MFMA    */
-#define BITCOS_KERNEL_SMALL_BATCH 4 /* BITCOS, 2..16 activation rows on MFMA                     */
+#define BITCOS_KERNEL_SMALL_BATCH 4 /* BITCOS, 2..16 activation rows on MFMA (and batch-1 rows   \
+                                       longer than the batch-1 tiles)                             */
 #define BITCOS_KERNEL_FIXED 5       /* five-trit or 2-bit                                        */
 typedef struct bitcos_launch_info {
   int32_t per_lane;        /* BITCOS: 32-weight words per lane; TRIT5: 128-blocks; BIT2: 16-weight words */

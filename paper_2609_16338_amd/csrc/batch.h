@@ -63,7 +63,8 @@ struct BatchHeader {
   int32_t any_xscale;    // some GEMV has activation scales
   int32_t any_grouped;   // some GEMV has group scales
   int32_t row_offsets;   // every BITCOS GEMV stores one sign offset per row
-  int32_t reserved[17];
+  int32_t small_batch;   // m == 1 rows longer than any batch-1 tile: the small-batch kernel
+  int32_t reserved[16];
 };
 static_assert(sizeof(BatchHeader) == 128, "BatchHeader is 128 bytes");
 
@@ -103,6 +104,11 @@ inline int gemv_rows(GemvEntry gemv, const bitcos_layout* L, const void* blob_de
   }
   return BITCOS_OK;
 }
+
+// Batch-1 layouts with rows longer than any batch-1 tile (the activations
+// of a lane live in VGPRs: bf16 K > 16384, int8 K > 32768) run the
+// small-batch kernel with one activation row, when it takes the layout.
+bool batch1_on_small_batch(const bitcos_layout* L, int32_t x_dtype);
 
 // Count a descriptor's units as the small-batch kernel's units.
 inline void to_mfma_units(GemvDesc* d) { d->units = (d->n + kMfmaUnitRows - 1) / kMfmaUnitRows; }

@@ -57,8 +57,8 @@ int make_desc(const bitcos_layout* L, const void* blob_dev, const void* x_dev, c
   if (!blob_dev || !x_dev || !y_dev) return BITCOS_E_ARG;
   if (xscale_dev && L->k % 128) return BITCOS_E_ARG;
   int per_lane = 0, seg = 0, rows = 0;
-  if (m == 1 || !mfma_layout_ok(L)) {  // the small-batch kernel has no tile limit on K
-    st = tile_for(L, x_dtype, &per_lane, &seg, &rows);
+  if (!mfma_layout_ok(L) || (m == 1 && !batch1_on_small_batch(L, x_dtype))) {
+    st = tile_for(L, x_dtype, &per_lane, &seg, &rows);  // the small-batch kernel has no tile limit on K
     if (st) return st;
   }
   memset(d, 0, sizeof(*d));
@@ -99,6 +99,12 @@ int make_desc(const bitcos_layout* L, const void* blob_dev, const void* x_dev, c
   return BITCOS_OK;
 }
 
+bool batch1_on_small_batch(const bitcos_layout* L, int32_t x_dtype) {
+  if (!L || !mfma_layout_ok(L)) return false;
+  int per_lane = 0, seg = 0, rows = 0;
+  return tile_for(L, x_dtype, &per_lane, &seg, &rows) == BITCOS_E_UNSUPPORTED;
+}
+
 bool to_step_units(GemvDesc* d, int rows) {
   if (d->unit_rows < 1 || rows % d->unit_rows) return false;
   d->offset_stride = rows / d->unit_rows;
@@ -107,7 +113,7 @@ bool to_step_units(GemvDesc* d, int rows) {
 }
 
 static int launch(const BatchHeader& h, const GemvDesc* table_dev, const GemvDesc& one, void* stream) {
-  if (h.m > 1) return launch_bitcos_mfma(h, table_dev, one, stream);
+  if (h.m > 1 || h.small_batch) return launch_bitcos_mfma(h, table_dev, one, stream);
   return h.format == BITCOS_FMT_BITCOS ? launch_bitcos(h, table_dev, one, stream)
                                        : launch_fixed(h, table_dev, one, stream);
 }
@@ -162,7 +168,8 @@ int bitcos_batch_build(int32_t count, int32_t m, const bitcos_layout* layouts, c
   h.m = m;
   bitcos::GemvDesc* descs =
       reinterpret_cast<bitcos::GemvDesc*>(static_cast<uint8_t*>(table) + sizeof(bitcos::BatchHeader));
-  if (m > 1) {
+  if (m > 1 || bitcos::batch1_on_small_batch(&layouts[0], x_dtype)) {
+    h.small_batch = m == 1;
     int st = bitcos::build_small_batch(count, m, layouts, blobs_dev, x_dev, xscale_dev, y_dev, &h, descs);
     if (st) return st;
     memcpy(table, &h, sizeof(h));
@@ -227,7 +234,8 @@ int bitcos_describe(const bitcos_layout* L, int32_t m, int32_t x_dtype, bitcos_l
   int st = bitcos::check_layout(L);
   if (st) return st;
   if (x_dtype != BITCOS_X_I8 && x_dtype != BITCOS_X_BF16) return BITCOS_E_ARG;
-  if (m > 1 && bitcos::mfma_layout_ok(L)) {  // small-batch kernel: 4 lanes per row, one word each per group
+  if (bitcos::mfma_layout_ok(L) && (m > 1 || bitcos::batch1_on_small_batch(L, x_dtype))) {
+    // small-batch kernel: 4 lanes per row, one word each per group
     const int64_t units = (L->n + bitcos::kMfmaUnitRows - 1) / bitcos::kMfmaUnitRows;
     out->per_lane = 1;
     out->seg_lanes = 4;

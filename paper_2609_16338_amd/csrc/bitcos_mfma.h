@@ -1,7 +1,10 @@
 // BITCOS GEMV for a small batch of activation rows (2 <= M <= 16) on the
 // matrix cores.  Decode cost per weight is the same at any batch size, so a
 // batch of M activation rows multiplies every decoded weight M times: one
-// MFMA takes a decoded weight tile against all (up to 16) rows at once.
+// MFMA takes a decoded weight tile against all (up to 16) rows at once.  It
+// also runs batch 1 (M = 1) for rows longer than the batch-1 kernels' tiles,
+// whose activations must fit a lane's registers; here they are read per
+// step, so K has no limit.
 //
 // Work unit: 32 output rows (two 16-row MFMA tiles) over the whole of K; a
 // wave walks its units in steps of four 128-weight scale groups.

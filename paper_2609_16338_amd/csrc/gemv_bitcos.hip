@@ -102,7 +102,8 @@ extern "C" int bitcos_gemv(const bitcos_layout* L, const void* blob_dev, int32_t
                            void* y_dev, int32_t y_mode, void* stream) {
   if (!L || L->format != BITCOS_FMT_BITCOS) return BITCOS_E_ARG;
   if (m < 1 || m > BITCOS_MAX_M) return BITCOS_E_ARG;
-  if (m > 1) {
+  // m > 1, or a batch-1 row longer than every batch-1 tile: the small-batch kernel.
+  if (m > 1 || bitcos::batch1_on_small_batch(L, x_dtype)) {
     if (!bitcos::mfma_layout_ok(L))
       return bitcos::gemv_rows(bitcos_gemv, L, blob_dev, m, x_dev, x_dtype, xscale_dev, y_dev, y_mode, stream);
     bitcos::GemvDesc d;
@@ -117,6 +118,7 @@ extern "C" int bitcos_gemv(const bitcos_layout* L, const void* blob_dev, int32_t
     h.x_dtype = x_dtype;
     h.y_mode = y_mode;
     h.m = m;
+    h.small_batch = m == 1;
     h.any_xscale = xscale_dev != nullptr;
     h.total_units = d.units;
     return bitcos::launch_bitcos_mfma(h, nullptr, d, stream);

@@ -14,7 +14,8 @@ static_assert(bitcos_k::kMfmaMaxBatch == BITCOS_MAX_M, "one MFMA tile holds ever
 namespace bitcos {
 
 int launch_bitcos_mfma(const BatchHeader& h, const GemvDesc* table_dev, const GemvDesc& one, void* stream) {
-  if (h.format != BITCOS_FMT_BITCOS || h.m < 2 || h.m > BITCOS_MAX_M) return BITCOS_E_UNSUPPORTED;
+  if (h.format != BITCOS_FMT_BITCOS || h.m < 1 || h.m > BITCOS_MAX_M) return BITCOS_E_UNSUPPORTED;
+  if (h.m == 1 && !h.small_batch) return BITCOS_E_UNSUPPORTED;
   if (h.total_units < 1 || h.total_units >= (int64_t(1) << 31)) return BITCOS_E_UNSUPPORTED;
   const bool bf16 = h.x_dtype == BITCOS_X_BF16;
   bitcos_k::MfmaFn fn = bitcos_k::pick_mfma(bf16, h.any_xscale != 0, table_dev != nullptr);

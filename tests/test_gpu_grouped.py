@@ -178,3 +178,63 @@ def test_repeated_runs_identical(k, group):
                 first = got.copy()
             else:
                 assert np.array_equal(got.view(np.uint32), first.view(np.uint32)), (kind, rep)
+
+
+# Batch-1 rows longer than every batch-1 tile: bf16 K > 16384 (a lane's
+# activations no longer fit its registers), int8 K > 32768.  They run the
+# small-batch kernel with one activation row.
+@pytest.mark.parametrize("k,kind,group", [(16512, "bf16", 128), (25600, "bf16", 0), (25600, "bf16", 128),
+                                          (32896, "int8", 0), (32896, "int8", 128)])
+def test_batch1_long_rows(k, kind, group):
+    n = 37
+    w, sc = inputs(n, k, 0.45, group, 30, lo=0.005, hi=0.05)
+    if kind == "bf16":
+        xb = wl.act_bf16(1, k, wl.rng_for(130, k))
+        y, L = run(N.FMT_BITCOS, w, sc, group, xb, "bf16")
+        assert _kernel(L, "bf16") == N.KERNEL_SMALL_BATCH
+        check_bf16(y, O.dense_gemv(w, sc, group, xb, x_is_bf16_bits=True), bf16_bound(w, sc, group, xb))
+        return
+    x = wl.act_int8(1, k, wl.rng_for(131, k))
+    y, L = run(N.FMT_BITCOS, w, sc, group, x, "int8")
+    assert _kernel(L, "int8") == N.KERNEL_SMALL_BATCH
+    if group == 0:
+        assert np.array_equal(y, O.dense_gemv(w, sc, 0, x))
+    else:
+        check_grouped(y, O.dense_gemv(w, sc, group, x), group_bound(w, sc, group, x))
+    y, _ = run(N.FMT_BITCOS, w, sc, group, x, "int8", y_mode=N.Y_I32_RAW)
+    assert np.array_equal(y, O.dense_gemv_raw(w, x).astype(np.int32))
+    q, a = O.quantize_activations(wl.act_bf16(1, k, wl.rng_for(132, k)))
+    y, _ = run(N.FMT_BITCOS, w, sc, group, q, "int8", xscale=a)
+    check_grouped(y, O.dense_gemv(w, sc, group, q, a), group_bound(w, sc, group, q, a))
+
+
+def test_batch1_long_rows_batch_table():
+    """Long-row GEMVs of one batch (m = 1, the small-batch kernel), twice: same bits."""
+    k = 25600
+    specs = [(48, 0.45), (5, 0.0), (131, 0.6)]
+    layouts, blobs, xs, ys, refs, bounds = [], [], [], [], [], []
+    for i, (n, z) in enumerate(specs):
+        w, sc = inputs(n, k, z, 128, 800 + i, lo=0.005, hi=0.05)
+        x = wl.act_bf16(1, k, wl.rng_for(801, i))
+        refs.append(O.dense_gemv(w, sc, 128, x, x_is_bf16_bits=True))
+        bounds.append(bf16_bound(w, sc, 128, x))
+        L, blob = api.plan_and_pack(N.FMT_BITCOS, w, sc, 128)
+        assert _kernel(L, "bf16") == N.KERNEL_SMALL_BATCH
+        layouts.append(L)
+        blobs.append(torch.from_numpy(blob).cuda())
+        xs.append(to_dev_x(x, "bf16").reshape(-1))
+        ys.append(torch.full((n,), -7.0, dtype=torch.float32, device="cuda"))
+    say("long-row batch", k)
+    b = api.Batch(layouts, blobs, xs, ys)
+    first = None
+    for rep in range(2):
+        b.run()
+        torch.cuda.synchronize()
+        got = [y.cpu().numpy()[None] for y in ys]
+        for g, ref, bound in zip(got, refs, bounds):
+            check_bf16(g, ref, bound)
+        if first is None:
+            first = [g.copy() for g in got]
+        else:
+            for g, f in zip(got, first):
+                assert np.array_equal(g.view(np.uint32), f.view(np.uint32))

@@ -244,6 +244,14 @@ def test_describe_kernel_choice():
     # a unit that does not divide the wave step: the general kernel
     assert kind(0, 3) == N.KERNEL_GENERAL
     assert kind(128, 3) == N.KERNEL_GENERAL
+    # rows longer than every batch-1 tile (bf16 K > 16384, int8 K > 32768): the small-batch kernel at m = 1
+    assert kind(0, 1, k=16384) == N.KERNEL_MATRIX
+    assert kind(128, 1, k=16512) == N.KERNEL_SMALL_BATCH
+    assert kind(0, 1, k=25600) == N.KERNEL_SMALL_BATCH
+    assert kind(0, 1, k=25600, x=N.X_I8) == N.KERNEL_MATRIX
+    assert kind(128, 1, k=32896, x=N.X_I8) == N.KERNEL_SMALL_BATCH
+    with pytest.raises(N.BitcosError):
+        kind(0, 2, k=25600)  # several rows per offset: no kernel takes such rows
     # small batch and the baselines
     assert kind(0, 1, m=4) == N.KERNEL_SMALL_BATCH
     assert kind(0, 0, fmt=N.FMT_TRIT5) == N.KERNEL_FIXED
