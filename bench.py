@@ -182,6 +182,8 @@ def make_step(entries, acts, kind):
 
 
 def capture(step):
+    """A graph of one call of `step`, holding `step` (and through it the batch
+    tables and outputs whose device addresses the graph's launches carry)."""
     import torch
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())
@@ -193,6 +195,7 @@ def capture(step):
     with torch.cuda.graph(g):
         step()
     torch.cuda.synchronize()
+    g.launched = step
     return g
 
 
