@@ -440,7 +440,7 @@ __global__ void __launch_bounds__(diag_threads(W, BF16)) bitcos_diag_kernel(cons
   };
 
   // Decode of one step; `next` issues the following step's loads right after
-  // this step's wait.  The step's loads (presence words, row offsets and the
+  // this step's wait (and the activations of a GEMV the wave enters).  The step's loads (presence words, row offsets and the
   // sign block staged into LDS) are waited for all at once: a sign block's
   // LDS-DMA may complete after vector-memory loads issued behind it, so a
   // counted vmcnt wait does not cover it.  With the next step's loads issued
@@ -450,9 +450,11 @@ __global__ void __launch_bounds__(diag_threads(W, BF16)) bitcos_diag_kernel(cons
   auto decode = [&](auto stage_c, auto&& next) {
     constexpr int k = decltype(stage_c)::value;
     const FastStep& s = st[k];
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    wait_vmem_all();
     flush_store();
-    next();
+    // Entering another GEMV: its activations, loaded and waited for before
+    // the next step's loads are issued, so that no wait inside the step
+    // covers those loads.
     if (s.di != xdi) {
       xdi = s.di;
       const auto& g = desc_at<TABLE>(a, xdi);
@@ -469,7 +471,9 @@ __global__ void __launch_bounds__(diag_threads(W, BF16)) bitcos_diag_kernel(cons
       mode = g.mode;
       tensor_scale = half_bits_to_float(gp_u16(g.scales)[0]);
       ry = make_rsrc(g.y, g.y_bytes);
+      wait_vmem_all();
     }
+    next();
     const uint32_t* scr32 = reinterpret_cast<const uint32_t*>(stage_buf(stage_c));
     if (ragged) {
 #pragma unroll

@@ -258,10 +258,12 @@ __global__ void __launch_bounds__(fast_threads(W, BF16)) bitcos_fast_kernel(cons
   auto decode = [&](auto stage_c, auto&& next) {
     constexpr int k = decltype(stage_c)::value;
     const FastStep& s = st[k];
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    wait_vmem_all();
     flush_store();
-    next();
-    if (s.di != xdi) {  // entering another GEMV: its activations and scales
+    // Entering another GEMV: its activations and scales, loaded and waited
+    // for before the next step's loads are issued, so that no wait inside
+    // the step covers those loads.
+    if (s.di != xdi) {
       xdi = s.di;
       const auto& g = desc_at<TABLE>(a, xdi);
       nwl = g.upr - w0;
@@ -282,7 +284,9 @@ __global__ void __launch_bounds__(fast_threads(W, BF16)) bitcos_fast_kernel(cons
       }
       tensor_scale = half_bits_to_float(gp_u16(g.scales)[0]);
       ry = make_rsrc(g.y, g.y_bytes);
+      wait_vmem_all();
     }
+    next();
     const uint32_t* scr32 = reinterpret_cast<const uint32_t*>(stage_buf(stage_c));
     // Words past the end of a row (ragged tiles only) count as empty.
     if (ragged) {

@@ -49,6 +49,19 @@ __device__ __forceinline__ uint16_t ld16(rsrc_t r, uint32_t off) {
   return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
 }
 
+// Waits until every vector-memory access of the wave has completed: vmcnt 0,
+// the LDS/scalar and export counts untouched (s_waitcnt immediate 0x0F70 on
+// gfx9).  Issued through the builtin rather than inline asm so that the
+// compiler's own wait insertion sees it: registers those accesses filled are
+// then known to be ready, and no counted wait for them is placed after loads
+// issued later (which would also wait for those later loads).  The empty asm
+// keeps memory accesses (LDS reads of data staged by LDS-DMA) from moving
+// above it.
+__device__ __forceinline__ void wait_vmem_all() {
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+  asm volatile("" ::: "memory");
+}
+
 constexpr int kWave = 64;
 constexpr int kBlock = 256;  // 4 waves per workgroup
 
