@@ -14,6 +14,12 @@ beside it).  value = sum of BITCOS payload bytes (bitmap + signs + scales) /
 step time.  The same step over the five-trit and 2-bit layouts of the same
 weights gives the same-GPU speedups.
 
+--workload and --batch M select the other layer sets and M activation rows
+per GEMV (BITCOS runs M > 1 in one launch per tile on its small-batch
+kernel; the five-trit and 2-bit layouts have no such kernel and take M
+batch-1 launches, as their entry points do).  A baseline with no kernel for
+a set (bf16 activations on rows longer than 16384) is reported as null.
+
 Prints ONE JSON line.  roofline: the dominant launch (the K = 2560 GEMVs of
 the step, one persistent launch) timed alone, from a graph of ten back-to-back
 launches; achieved = its
@@ -41,6 +47,7 @@ sys.path.insert(0, ROOT)
 import workloads as wl  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
+FMT_NAMES = {1: "bitcos", 2: "trit5", 3: "bit2"}
 METRIC = "ternary GEMV effective weight GB/s (% of 8 TB/s HBM peak); speedup vs 5-trit"
 
 
@@ -50,6 +57,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--workload", default="bitnet2b_layers")
+    ap.add_argument("--batch", type=int, default=1,
+                    help="activation rows per GEMV (1..16); BITCOS runs M > 1 on its small-batch kernel")
     ap.add_argument("--layers", type=int, default=0, help="0 = the workload's layer count")
     ap.add_argument("--copies", type=int, default=2,
                     help="device copies of the layer set, replayed in turn (2 x 411 MB > 2 x the 256 MB Infinity Cache)")
@@ -126,49 +135,77 @@ def build_set(wk, layers, fmts, threads):
     return packed
 
 
-def activations(wk, kinds):
-    """Per distinct K: device activations (bf16, and int8 + per-group scales via the library)."""
+def activations(wk, kinds, m=1):
+    """Per distinct K: device activations [m, k] (bf16, and int8 + per-group
+    scales via the library)."""
     import torch
 
     from paper_2609_16338_amd import api
 
     acts = {}
     for k in sorted({s.k for s in wk.matrices}):
-        xb = wl.activation_inputs(wk.cid, "bf16", 1, k)
+        xb = wl.activation_inputs(wk.cid, "bf16", m, k)
         xbd = torch.from_numpy(xb.view(np.int16)).view(torch.bfloat16).cuda()
         acts[("bf16", k)] = (xbd, None)
         if "int8" in kinds:
-            q = torch.empty((1, k), dtype=torch.int8, device="cuda")
-            a = torch.empty((1, k // 128), dtype=torch.float32, device="cuda")
+            q = torch.empty((m, k), dtype=torch.int8, device="cuda")
+            a = torch.empty((m, k // 128), dtype=torch.float32, device="cuda")
             api.quantize_activations(xbd, q, a)
             acts[("int8", k)] = (q, a)
     torch.cuda.synchronize()
     return acts
 
 
+def supported(entries, kind, m=1):
+    """Whether the library has a kernel for every GEMV of the step at m rows
+    (formats without a small-batch kernel run m > 1 as m batch-1 launches)."""
+    from paper_2609_16338_amd import _native as N
+    from paper_2609_16338_amd import api
+
+    xd = N.X_BF16 if kind == "bf16" else N.X_I8
+    for e in entries:
+        mm = m if e[3].format == N.FMT_BITCOS else 1
+        try:
+            api.describe(e[3], mm, xd)
+        except N.BitcosError:
+            return False
+    return True
+
+
 def make_batches(entries, acts, kind):
-    """One persistent launch per tile: the step's GEMVs grouped by kernel tile."""
+    """One persistent launch per tile: the step's GEMVs grouped by kernel tile.
+
+    With m activation rows, BITCOS takes all m in one launch (small-batch
+    kernel); the five-trit and 2-bit layouts, which have no small-batch
+    kernel, take m batch-1 launches per tile, one per activation row, as
+    their m > 1 entry points do."""
     import torch
 
     from paper_2609_16338_amd import _native as N
     from paper_2609_16338_amd import api
 
     xd = N.X_BF16 if kind == "bf16" else N.X_I8
+    m = next(iter(acts.values()))[0].shape[0]
+    rows_per_launch = m if entries[0][3].format == N.FMT_BITCOS else 1
     groups = {}
     for e in entries:
-        L = e[3]
-        info = api.describe(L, 1, xd)
-        groups.setdefault((info.per_lane, info.seg_lanes), []).append(e)
+        info = api.describe(e[3], rows_per_launch, xd)
+        groups.setdefault((info.kernel, info.per_lane, info.seg_lanes), []).append(e)
     batches = []
     for tile, ents in sorted(groups.items(), key=lambda kv: -sum(e[3].n * e[3].k for e in kv[1])):
-        ys = [torch.empty(e[3].n, dtype=torch.float32, device="cuda") for e in ents]
-        xs = [acts[(kind, e[2].k)][0].reshape(-1) for e in ents]
-        xss = [acts[(kind, e[2].k)][1] for e in ents]
-        b = api.Batch([e[3] for e in ents], [e[4] for e in ents], xs, ys,
-                      xss if any(v is not None for v in xss) else None)
-        b.tile = tile
-        b.entries = ents
-        batches.append(b)
+        ys = [torch.empty((m, e[3].n), dtype=torch.float32, device="cuda") for e in ents]
+        for r0 in range(0, m, rows_per_launch):
+            r1 = r0 + rows_per_launch
+            xs = [acts[(kind, e[2].k)][0][r0:r1] for e in ents]  # [rows, k]: the batch takes rows from its shape
+            xs = [x.reshape(-1) if rows_per_launch == 1 else x for x in xs]
+            xss = [acts[(kind, e[2].k)][1] for e in ents]
+            xss = [None if v is None else v[r0:r1].reshape(-1) for v in xss]
+            b = api.Batch([e[3] for e in ents], [e[4] for e in ents], xs, [y[r0:r1].reshape(-1) for y in ys],
+                          xss if any(v is not None for v in xss) else None)
+            b.tile = tile[1:]
+            b.entries = ents
+            b.outputs = ys
+            batches.append(b)
     return batches
 
 
@@ -479,23 +516,37 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     wk = wl.WORKLOADS[args.workload]
     layers = args.layers or wk.layers
+    m = args.batch
+    if not 1 <= m <= 16:
+        print(json.dumps({"error": "--batch must be in 1..16"}))
+        sys.exit(2)
     fmts = [N.FMT_BITCOS] + ([] if args.no_baselines else [N.FMT_TRIT5, N.FMT_BIT2])
     t0 = time.perf_counter()
     packed = build_set(wk, layers, fmts, args.threads)
-    acts = activations(wk, ("bf16", "int8"))
+    acts = activations(wk, ("bf16", "int8"), m)
     prep_s = time.perf_counter() - t0
     print(f"[bench] packed {layers} layers x {len(wk.matrices)} matrices in {prep_s:.1f} s", file=sys.stderr, flush=True)
 
     payload = {fmt: sum(e[3].payload_bits for e in ents) / 8 for fmt, ents in packed.items()}
     weights = sum(e[3].n * e[3].k for e in packed[N.FMT_BITCOS])
     res = {}
+    unsupported = {}
     copies = max(1, args.copies)
     bitcos_sets = None
+    warmed = False
     for fmt in fmts:
         sets = device_copies(packed[fmt], copies)
         for kind in ("bf16", "int8"):
+            if not supported(packed[fmt], kind, m):
+                if fmt == N.FMT_BITCOS:
+                    raise SystemExit(f"no BITCOS kernel for this set with {kind} activations at batch {m}")
+                res[(fmt, kind)] = None
+                unsupported[f"{FMT_NAMES[fmt]}_{kind}"] = "no kernel for rows this long (K > 16384 with bf16 activations)"
+                print(f"[bench] fmt={fmt} {kind}: no kernel for this set, skipped", file=sys.stderr, flush=True)
+                continue
             gs = [capture(make_step(st, acts, kind)[0]) for st in sets]
-            if not res:
+            if not warmed:
+                warmed = True
                 n, wms = warm_device(gs[0])
                 print(f"[bench] device warm-up: {n} untimed replays in {wms:.0f} ms", file=sys.stderr, flush=True)
             ms, wall = time_graphs(gs, args.steps, args.warmup)
@@ -519,7 +570,7 @@ def main():
     gg = capture(lambda: [tops[i % len(tops)].run() for i in range(reps)])
     ms_g, _ = time_graph(gg, args.steps, args.warmup)
     per_launch_us = ms_g * 1e3 / reps
-    alg_bytes = sum(e[3].payload_bits / 8 + e[3].k * 2 + e[3].n * 4 for e in top.entries)
+    alg_bytes = sum(e[3].payload_bits / 8 + m * (e[3].k * 2 + e[3].n * 4) for e in top.entries)
     achieved = alg_bytes / (per_launch_us * 1e-6) / 1e9
     ms = res[(N.FMT_BITCOS, "bf16")]
     value = payload[N.FMT_BITCOS] / (ms * 1e-3) / 1e9
@@ -541,8 +592,8 @@ def main():
                         f"k,v {wk.matrices[1].n}x{wk.matrices[1].k}; gate,up {wk.matrices[4].n}x{wk.matrices[4].k}; "
                         f"down {wk.matrices[6].n}x{wk.matrices[6].k}}}, z={wk.matrices[0].z} iid, "
                         f"{'per-tensor' if wk.matrices[0].group == 0 else 'group-128'} fp16 scales, "
-                        "bf16 x ~ N(0,1), batch 1",
-            "global_batch": 1,
+                        f"bf16 x ~ N(0,1), batch {m}",
+            "global_batch": m,
             "layers": layers,
             "gemvs_per_step": len(packed[N.FMT_BITCOS]),
             "weights_per_step": weights,
@@ -553,26 +604,32 @@ def main():
         "weights_per_s": float(f"{weights / (ms * 1e-3):.4g}"),
         "bpw_payload": round(payload[N.FMT_BITCOS] * 8 / weights, 5),
     }
-    if N.FMT_TRIT5 in fmts:
-        out["speedup_vs_trit5"] = round(res[(N.FMT_TRIT5, "bf16")] / ms, 4)
-        out["speedup_vs_bit2"] = round(res[(N.FMT_BIT2, "bf16")] / ms, 4)
-        out["baselines_us_per_step"] = {
-            "trit5_bf16": round(res[(N.FMT_TRIT5, "bf16")] * 1e3, 2),
-            "bit2_bf16": round(res[(N.FMT_BIT2, "bf16")] * 1e3, 2),
-            "trit5_int8": round(res[(N.FMT_TRIT5, "int8")] * 1e3, 2),
-            "bit2_int8": round(res[(N.FMT_BIT2, "int8")] * 1e3, 2),
-        }
+    def ratio(fmt, kind, t):
+        v = res.get((fmt, kind))
+        return None if v is None else round(v / t, 4)
+
     ms8 = res[(N.FMT_BITCOS, "int8")]
+    if N.FMT_TRIT5 in fmts:
+        out["speedup_vs_trit5"] = ratio(N.FMT_TRIT5, "bf16", ms)
+        out["speedup_vs_bit2"] = ratio(N.FMT_BIT2, "bf16", ms)
+        out["baselines_us_per_step"] = {
+            f"{FMT_NAMES[f]}_{kind}": None if res[(f, kind)] is None else round(res[(f, kind)] * 1e3, 2)
+            for f in (N.FMT_TRIT5, N.FMT_BIT2) for kind in ("bf16", "int8")}
+        if m > 1:
+            out["baselines_note"] = f"no small-batch kernel: {m} batch-1 launches per tile and step"
+        if unsupported:
+            out["baselines_unsupported"] = unsupported
     out["int8_variant"] = {
         "value": round(payload[N.FMT_BITCOS] / (ms8 * 1e-3) / 1e9, 2),
         "ms_per_step": round(ms8, 5),
-        "speedup_vs_trit5": round(res[(N.FMT_TRIT5, "int8")] / ms8, 4) if N.FMT_TRIT5 in fmts else None,
-        "speedup_vs_bit2": round(res[(N.FMT_BIT2, "int8")] / ms8, 4) if N.FMT_TRIT5 in fmts else None,
+        "speedup_vs_trit5": ratio(N.FMT_TRIT5, "int8", ms8),
+        "speedup_vs_bit2": ratio(N.FMT_BIT2, "int8", ms8),
     }
     # The kernel the launcher picks (all GEMVs of the launch share layout kind and tile).
-    kinds = {api.describe(e[3], 1, N.X_BF16).kernel for e in top.entries}
+    kinds = {api.describe(e[3], m, N.X_BF16).kernel for e in top.entries}
     kname = {N.KERNEL_MATRIX: "bitcos_diag_kernel", N.KERNEL_STREAMING: "bitcos_fast_kernel",
-             N.KERNEL_GENERAL: "bitcos_gemv_kernel"}.get(kinds.pop(), "?") if len(kinds) == 1 else "mixed"
+             N.KERNEL_GENERAL: "bitcos_gemv_kernel", N.KERNEL_SMALL_BATCH: "bitcos_mfma_kernel",
+             }.get(kinds.pop(), "?") if len(kinds) == 1 else "mixed"
     out["roofline"] = {
         "bound": "hbm",
         "achieved": round(achieved, 2),

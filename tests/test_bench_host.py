@@ -70,3 +70,23 @@ def test_device_copies_share_layouts_and_clone_blobs():
         assert [e[3] for e in st] == ["L0", "L1"]
         assert [e[4].tag for e in st] == ["b0'", "b1'"]
         assert all(a[4] is not b[4] for a, b in zip(st, entries))
+
+
+def test_supported_reports_baselines_without_a_long_row_kernel():
+    """bf16 rows longer than 16384 have a BITCOS kernel at batch 1 (the
+    small-batch kernel) but no five-trit or 2-bit kernel; int8 rows of that
+    length have all three."""
+    np = pytest.importorskip("numpy")
+    api = pytest.importorskip("paper_2609_16338_amd.api")
+    from paper_2609_16338_amd import _native as N
+
+    rng = np.random.default_rng(5)
+    k = 25600
+    w = rng.integers(-1, 2, size=(3, k)).astype(np.int8)
+    sc = np.full((3, k // 128), 0.01, np.float16)
+    for fmt, bf16_ok in ((N.FMT_BITCOS, True), (N.FMT_TRIT5, False), (N.FMT_BIT2, False)):
+        L, _ = api.plan_and_pack(fmt, w, sc, 128)
+        entries = [(0, 6, None, L, None)]
+        assert bench.supported(entries, "bf16", 1) is bf16_ok
+        assert bench.supported(entries, "int8", 1)
+        assert bench.supported(entries, "bf16", 4) is bf16_ok  # baselines at m > 1: batch-1 launches
