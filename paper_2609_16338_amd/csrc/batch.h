@@ -110,8 +110,12 @@ inline int gemv_rows(GemvEntry gemv, const bitcos_layout* L, const void* blob_de
 // small-batch kernel with one activation row, when it takes the layout.
 bool batch1_on_small_batch(const bitcos_layout* L, int32_t x_dtype);
 
-// Count a descriptor's units as the small-batch kernel's units.
-inline void to_mfma_units(GemvDesc* d) { d->units = (d->n + kMfmaUnitRows - 1) / kMfmaUnitRows; }
+// Count a descriptor in the small-batch kernel's steps: units of 32 rows,
+// each K / 512 steps (four 128-weight groups per step).  The kernel splits a
+// launch's steps evenly over its waves.
+inline void to_mfma_units(GemvDesc* d) {
+  d->units = static_cast<int64_t>((d->n + kMfmaUnitRows - 1) / kMfmaUnitRows) * ((d->ngroups + 3) / 4);
+}
 
 // Tile (per-lane units, lanes per row) the given layout runs with.
 int tile_for(const bitcos_layout* L, int32_t x_dtype, int* per_lane, int* seg, int* rows);

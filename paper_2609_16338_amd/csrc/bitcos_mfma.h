@@ -7,7 +7,11 @@
 // step, so K has no limit.
 //
 // Work unit: 32 output rows (two 16-row MFMA tiles) over the whole of K; a
-// wave walks its units in steps of four 128-weight scale groups.
+// wave walks its units in steps of four 128-weight scale groups.  A launch
+// counts its GEMVs in steps (a unit of a K-long row is K / 512 steps), and
+// each wave takes the units that start inside its equal share of the steps,
+// so GEMVs of different K in one launch leave no wave with several times the
+// others' work.
 //   * Lane l works on row n = l % 16 of each tile and, in every group, on its
 //     32-weight word g = l / 16, so the four lane groups of a row cover one
 //     group together and an MFMA never mixes two scale groups.
@@ -73,19 +77,21 @@ __global__ void __launch_bounds__(kMfmaThreads) bitcos_mfma_kernel(const KernelA
   const int lane = threadIdx.x & 63;
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wave = __builtin_amdgcn_readfirstlane(blockIdx.x * WPB + wv);
+  // The wave's share of the launch's steps: [S0, S1).
   const int total = static_cast<int>(a.total_units);
   const int nwaves = static_cast<int>(gridDim.x) * WPB;
   const int per = (total + nwaves - 1) / nwaves;
-  const int U0 = per * wave;
-  const int U1 = min(U0 + per, total);
-  if (U0 >= U1) return;
+  const int S0 = per * wave;
+  const int U1 = min(S0 + per, total);
+  if (S0 >= U1) return;
 
   const int nr = lane & 15;
   const int g = lane >> 4;
   const int cp = lane & (NC - 1);
   uint32_t* const stage = sstage + wv * (kMfmaRows * kSignStride);
 
-  // ---- fetch side: the GEMV whose step is being fetched
+  // ---- fetch side: the GEMV whose step is being fetched; fbeg / fend: its
+  // first step in the launch and one past its last, fC: steps per unit.
   int fdi = 0, fbeg = 0, fend = 0, fC = 1, fG = 1, fk = 0, fupr = 0;
   rsrc_t rb = make_rsrc(nullptr, 0), rg = rb, rs = rb, rx = rb, rxs = rb;
   auto fetch_enter = [&](int d) {
@@ -104,29 +110,44 @@ __global__ void __launch_bounds__(kMfmaThreads) bitcos_mfma_kernel(const KernelA
     const bool xs = XS && (D.mode & kModeXscale);
     rxs = make_rsrc(xs ? D.xscale : nullptr, xs ? D.x_bytes / (32u * ELEM) : 0u);
   };
-  // Sign offsets of the lane's rows in unit U of the launch (U in the GEMV
-  // being fetched or the next one).
-  auto unit_offsets = [&](int U, uint32_t (&o)[RT]) {
-    const bool in = U < U1;
-    const int d = (U < fend) ? fdi : min(fdi + 1, a.count - 1);
+  // Sign offsets of the lane's rows in the unit starting at row0 of GEMV d
+  // (nothing when `in` is false).
+  auto load_offsets = [&](int d, int row0, bool in, uint32_t (&o)[RT]) {
     const auto& D = desc_at<TABLE>(a, d);
     const rsrc_t ro = make_rsrc(D.offsets, static_cast<uint32_t>(D.n + 1) * 4u);
-    const int row0 = (U - static_cast<int>(D.unit_begin)) * kMfmaRows;
 #pragma unroll
     for (int r = 0; r < RT; ++r)
       o[r] = ld32(ro, in ? static_cast<uint32_t>(row0 + kMfmaTile * r + nr) * 4u : kOOB);
   };
+  // ... of the unit after unit u of the GEMV being fetched: unit u + 1, or the
+  // next GEMV's first unit; read only if that unit starts inside the wave's
+  // share (past the wave's last unit, u may be stale: nothing is read then,
+  // or rows of a unit of the same GEMV, inside its buffer, that go unused).
+  auto next_unit_offsets = [&](int u, uint32_t (&o)[RT]) {
+    const int start = fbeg + (u + 1) * fC;
+    const bool same = start < fend;
+    load_offsets(same ? fdi : min(fdi + 1, a.count - 1), same ? (u + 1) * kMfmaRows : 0, start < U1, o);
+  };
 
+  // First unit: the first one of the launch to start at or after S0.
+  int u0 = 0;
   {
     int lo = 0;
-    if constexpr (TABLE) {  // last descriptor with unit_begin <= U0
+    if constexpr (TABLE) {  // last descriptor with unit_begin <= S0
       int hi = a.count;
       while (hi - lo > 1) {
         const int mid = (lo + hi) >> 1;
-        if (((CDesc*)a.table)[mid].unit_begin <= U0) lo = mid; else hi = mid;
+        if (((CDesc*)a.table)[mid].unit_begin <= S0) lo = mid; else hi = mid;
       }
     }
     fetch_enter(lo);
+    u0 = (S0 - fbeg + fC - 1) / fC;
+    if (fbeg + u0 * fC >= fend) {  // no unit of this GEMV starts in the share
+      if (fend >= U1) return;
+      fetch_enter(fdi + 1);
+      u0 = 0;
+    }
+    if (fbeg + u0 * fC >= U1) return;
   }
 
   // Step data: presence words, fp16 group scales and sign dwords of the
@@ -178,12 +199,13 @@ __global__ void __launch_bounds__(kMfmaThreads) bitcos_mfma_kernel(const KernelA
     MStep n = s;
     if (s.c + 1 < fC) {
       n.c = s.c + 1;
-    } else {
-      const int U = fbeg + s.unit + 1;
-      n.valid = U < U1;
-      if (n.valid && U >= fend) fetch_enter(fdi + 1);
+    } else {  // the next unit: u + 1, or the next GEMV's first; it is the wave's if it starts before U1
+      const int start = fbeg + (s.unit + 1) * fC;
+      const bool same = start < fend;
+      n.valid = start < U1;
+      if (n.valid && !same) fetch_enter(fdi + 1);
       n.di = fdi;
-      n.unit = U - fbeg;
+      n.unit = same ? s.unit + 1 : 0;
       n.c = 0;
     }
     n.last = n.c + 1 == fC;
@@ -211,15 +233,15 @@ __global__ void __launch_bounds__(kMfmaThreads) bitcos_mfma_kernel(const KernelA
   // ---- prologue
   MStep fs;
   fs.di = fdi;
-  fs.unit = U0 - fbeg;
+  fs.unit = u0;
   fs.c = 0;
   fs.last = fC == 1;
   fs.valid = true;
   Slot cur, nxt;
   uint32_t offn[RT];
-  unit_offsets(U0, cur.pos);
+  load_offsets(fdi, u0 * kMfmaRows, true, cur.pos);
   issue(fs, cur);
-  unit_offsets(U0 + 1, offn);
+  next_unit_offsets(u0, offn);
 #pragma unroll
   for (int q = 0; q < 4; ++q) issue_x(fs, q);
 
@@ -260,16 +282,15 @@ __global__ void __launch_bounds__(kMfmaThreads) bitcos_mfma_kernel(const KernelA
       stot[r] = cum - (cur.pos[r] & 31u);
     }
 
-    // Fetch step t+1.
+    // Fetch step t+1.  offn holds the offsets of the unit after step t's:
+    // step t+1's own when it starts a unit.  They are reloaded every step,
+    // unconditionally: loads in a branch into a loop-carried register make
+    // the compiler copy them into place right away, a wait for every load
+    // in flight.
     fs = advance(cs);
-    if (fs.c == 0) {
 #pragma unroll
-      for (int r = 0; r < RT; ++r) nxt.pos[r] = offn[r];
-      unit_offsets(fbeg + fs.unit + 1, offn);
-    } else {
-#pragma unroll
-      for (int r = 0; r < RT; ++r) nxt.pos[r] = cur.pos[r] + stot[r];
-    }
+    for (int r = 0; r < RT; ++r) nxt.pos[r] = fs.c == 0 ? offn[r] : cur.pos[r] + stot[r];
+    next_unit_offsets(fs.unit, offn);
     issue(fs, nxt);
 
     // This step's sign dwords into the wave's LDS block.

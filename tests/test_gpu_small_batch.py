@@ -273,3 +273,47 @@ def test_full_size_qwen3_32b_small_batch(midx, m):
     x = wl.activation_inputs(wk.cid, "int8", m, spec.k)
     y, _ = run(N.FMT_BITCOS, w, sc, 128, x, "int8", y_mode=N.Y_I32_RAW)
     assert np.array_equal(y[:, rows], O.dense_gemv_raw(w[rows], x).astype(np.int32))
+
+
+def test_qwen3_32b_layer_in_one_small_batch_launch():
+    """All seven matrices of a Qwen3-32B-like layer (K = 5120 and 25600) in one
+    batch table at M = 4: the launch splits its steps (not its 32-row units)
+    over the waves, so waves start inside units and GEMVs of both row
+    lengths; every GEMV must still match the oracle on sampled rows, twice."""
+    wk = wl.WORKLOADS["qwen3_32b_layers"]
+    m = 4
+    mats = [wl.matrix_inputs(wk.cid, 1, i, spec) for i, spec in enumerate(wk.matrices)]
+    for kind in ("int8", "bf16"):
+        layouts, blobs, xs, ys, xsrc = [], [], [], [], []
+        for i, (spec, (w, sc)) in enumerate(zip(wk.matrices, mats)):
+            L, blob = api.plan_and_pack(N.FMT_BITCOS, w, sc, 128)
+            x = wl.activation_inputs(wk.cid, kind, m, spec.k, salt=i)
+            layouts.append(L)
+            blobs.append(torch.from_numpy(blob).cuda())
+            xs.append(to_dev_x(x, kind))
+            xsrc.append(x)
+            ys.append(torch.full((m, spec.n), -7.0, dtype=torch.float32, device="cuda"))
+        say("qwen3-32b layer, one small-batch launch", kind)
+        ymode = N.Y_I32_RAW if kind == "int8" else N.Y_F32
+        if kind == "int8":
+            ys = [torch.full((m, spec.n), -7, dtype=torch.int32, device="cuda") for spec in wk.matrices]
+        b = api.Batch(layouts, blobs, xs, ys, y_mode=ymode)
+        assert b.m == m
+        first = None
+        for rep in range(2):
+            b.run()
+            torch.cuda.synchronize()
+            got = [y.cpu().numpy() for y in ys]
+            for i, (spec, (w, sc), x, g) in enumerate(zip(wk.matrices, mats, xsrc, got)):
+                rows = sampled_rows(spec.n, 24, 70 + i)
+                if kind == "int8":
+                    assert np.array_equal(g[:, rows], O.dense_gemv_raw(w[rows], x).astype(np.int32)), spec.name
+                else:
+                    scr = sc.reshape(spec.n, -1)[rows].reshape(-1)
+                    check_bf16(g[:, rows], O.dense_gemv(w[rows], scr, 128, x, x_is_bf16_bits=True),
+                               bf16_bound(w[rows], scr, 128, x))
+            if first is None:
+                first = [g.copy() for g in got]
+            else:
+                for g, f in zip(got, first):
+                    assert np.array_equal(g.view(np.uint32), f.view(np.uint32))
