@@ -28,8 +28,9 @@ constexpr int kMaxWords2Bf16 = 16; // 2-bit: 8 dwords per word
 
 // Pick the tile that leaves the fewest lanes idle for `units_per_row` units
 // split into chunks of at most `max_per_lane`; ties go to the smaller
-// per-lane count (fewer registers).  Returns false if no tile fits.
-inline bool choose_tile(int units_per_row, int max_per_lane, Tile* t) {
+// per-lane count (fewer registers), or with `wide` to the larger one (more
+// rows per wave step).  Returns false if no tile fits.
+inline bool choose_tile(int units_per_row, int max_per_lane, Tile* t, bool wide = false) {
   double best = -1.0;
   Tile pick;
   for (int seg = 64; seg >= 4; seg /= 2) {
@@ -38,7 +39,8 @@ inline bool choose_tile(int units_per_row, int max_per_lane, Tile* t) {
     if (per_lane > max_per_lane) continue;
     int lanes = (units_per_row + per_lane - 1) / per_lane;
     double util = double(units_per_row) / double(seg * per_lane);
-    bool better = util > best + 1e-12 || (util > best - 1e-12 && per_lane < pick.per_lane);
+    bool better = util > best + 1e-12 ||
+                  (util > best - 1e-12 && (wide ? per_lane > pick.per_lane : per_lane < pick.per_lane));
     if (better) {
       best = util;
       pick.per_lane = per_lane;
@@ -52,9 +54,17 @@ inline bool choose_tile(int units_per_row, int max_per_lane, Tile* t) {
   return true;
 }
 
-// BITCOS tile for (K, activation type): words of 32 weights.
+// BITCOS tile for (K, activation type): words of 32 weights.  Among the
+// tiles of up to 8 words per lane that leave the fewest lanes idle, the
+// widest: a wave step then covers more rows and each lane more words, over
+// which the step's fixed work (prefix of the row's counts, sign offsets,
+// row sums) is spread; at K = 4096 eight words per lane on 16-lane rows run
+// the Qwen3-8B-like set 16 % (int8) and 8 % (bf16) faster than two words on
+// 64-lane rows, and sixteen words per lane are slower again.  Longer rows
+// (int8 K > 16384) take up to 16 words.
 inline bool bitcos_tile(int k, bool bf16, Tile* t) {
-  return choose_tile(k / 32, bf16 ? kMaxWordsBf16 : kMaxWordsI8, t);
+  constexpr int kWideWords = 8;
+  return choose_tile(k / 32, kWideWords, t, true) || choose_tile(k / 32, bf16 ? kMaxWordsBf16 : kMaxWordsI8, t);
 }
 
 // Default rows per sign offset: one, so every kernel (any rows per wave step,

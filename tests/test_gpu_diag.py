@@ -31,10 +31,10 @@ def _need_gpu():
 
 
 # K -> (words per lane, lanes per row): 96 -> (1, 4) ragged, 128 -> (1, 4),
-# 256 -> (1, 8), 512 -> (1, 16), 1024 -> (1, 32), 2048 -> (1, 64),
-# 2400 -> (5, 16) ragged, 2560 -> (5, 16), 4096 -> (2, 64), 5120 -> (5, 32),
-# 6912 -> (7, 32) ragged, 8192 -> (4, 64), 12288 -> (6, 64).
-KS = [96, 128, 256, 512, 1024, 2048, 2400, 2560, 4096, 5120, 6912, 8192, 12288]
+# 256 -> (2, 4), 512 -> (4, 4), 1024 -> (8, 4), 2048 -> (8, 8),
+# 2400 -> (5, 16) ragged, 2560 -> (5, 16), 4096 -> (8, 16), 5120 -> (5, 32),
+# 6912 -> (7, 32) ragged, 8192 -> (8, 32), 12288 -> (6, 64), 16384 -> (8, 64).
+KS = [96, 128, 256, 512, 1024, 2048, 2400, 2560, 4096, 5120, 6912, 8192, 12288, 16384]
 
 
 def _matrix_kernel(L, kind):
@@ -100,7 +100,7 @@ def test_matrix_kernel_extreme_activations_and_rows():
 def test_matrix_kernel_unit_rows_fallbacks(k, unit, expect):
     """Several rows per sign offset: at 16 or fewer lanes per row the streaming
     kernel runs, at 32 the matrix cores still do; a unit that does not divide
-    the wave step (8192: one row per step) takes the general kernel."""
+    the wave step (8192: two rows per step) takes the general kernel."""
     w, sc = inputs(37, k, 0.42, 0, 15)
     x = wl.act_int8(1, k, wl.rng_for(114, k))
     y, L = run(N.FMT_BITCOS, w, sc, 0, x, "int8", y_mode=N.Y_I32_RAW, unit=unit)

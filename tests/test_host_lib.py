@@ -212,7 +212,10 @@ def test_describe_small_batch():
 
 
 def test_describe_tiles():
-    for k, per_lane, seg in [(2560, 5, 16), (8192, 4, 64), (6912, 7, 32), (1024, 1, 32), (25600, 13, 64)]:
+    # fewest idle lanes first, then the widest tile up to 8 words per lane;
+    # int8 rows over 16384 take up to 16
+    for k, per_lane, seg in [(2560, 5, 16), (8192, 8, 32), (6912, 7, 32), (1024, 8, 4), (4096, 8, 16),
+                             (12288, 6, 64), (25600, 13, 64)]:
         w = np.zeros((8, k), np.int8)
         L = api.bitcos_plan(w, 128, 0)
         info = api.describe(L, 1, N.X_I8)
