@@ -26,8 +26,12 @@ launches; achieved = its
 algorithmic bytes (payload + 2 K activation bytes + 4 N output bytes per GEMV)
 per launch time, against the 8 TB/s HBM peak; traffic = its measured HBM
 bytes (FETCH_SIZE + WRITE_SIZE scaled by a plain copy's counters, stored under
-profiles/) while the kernel sources are unchanged.  cpu_baseline: the oracle's
-decode + dense GEMV on whole layer-0 matrices on the host, about 12 s of work.
+profiles/) while the kernel sources are unchanged; two_term: the launch's
+time and its bytes at peak HBM bandwidth, both in CU-cycles per 32 weights
+at the nominal 2.4 GHz, and which is larger.  sclk_mhz_under_load: the
+shader clock rocm-smi reads while that launch replays (untimed, after the
+timed runs).  cpu_baseline: the oracle's decode + dense GEMV on whole
+layer-0 matrices on the host, about 12 s of work.
 """
 
 from __future__ import annotations
@@ -298,6 +302,47 @@ def warm_device(g, min_ms=100.0):
     return n, (time.perf_counter() - t0) * 1e3
 
 
+def gpu_clock_under_load(g, seconds=1.5):
+    """The GPU's current shader clock (MHz, from rocm-smi) sampled while
+    `g` replays back to back for about `seconds`, untimed; None if the query
+    fails.  rocm-smi takes a good part of a second to start, longer than a
+    timed run, so the replays are queued first and the clock is read while
+    they execute."""
+    import re
+    import subprocess
+
+    import torch
+    t0 = time.perf_counter()
+    g.replay()
+    torch.cuda.synchronize()
+    one = max(time.perf_counter() - t0, 1e-5)
+    for _ in range(min(int(seconds / one), 20000)):
+        g.replay()
+    try:
+        out = subprocess.run(["rocm-smi", "-g", "--json"], capture_output=True, text=True, timeout=20).stdout
+        mhz = []
+        for card in json.loads(out).values():
+            if isinstance(card, dict):
+                mhz += [int(m) for key, v in card.items() if "sclk" in key.lower()
+                        for m in re.findall(r"(\d+)\s*mhz", str(v).lower())]
+        res = max(mhz) if mhz else None
+    except (OSError, subprocess.SubprocessError, ValueError):
+        res = None
+    torch.cuda.synchronize()
+    return res
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(wk, budget_s=12.0):
     """The oracle (decode + dense GEMV) on the host, on whole matrices of layer 0."""
     import oracle as O
@@ -329,6 +374,7 @@ def cpu_baseline(wk, budget_s=12.0):
         "value": round(done_bytes / t_total / 1e9, 4),
         "unit": "GB/s",
         "cores": int(cores),
+        "cpu_model": cpu_model(),
         "kind": "oracle",
         "sample": f"{mats} matrices of layer 0 of {wk.name} (decode + dense bf16 GEMV, "
                   f"{done_w / 1e6:.1f} M weights, {t_total:.1f} s)",
@@ -570,8 +616,15 @@ def main():
     gg = capture(lambda: [tops[i % len(tops)].run() for i in range(reps)])
     ms_g, _ = time_graph(gg, args.steps, args.warmup)
     per_launch_us = ms_g * 1e3 / reps
+    sclk = gpu_clock_under_load(gg)
     alg_bytes = sum(e[3].payload_bits / 8 + m * (e[3].k * 2 + e[3].n * 4) for e in top.entries)
     achieved = alg_bytes / (per_launch_us * 1e-6) / 1e9
+    # Two-term roofline of the launch in CU-cycles per 32 weights (nominal
+    # clock): its measured time against the time its bytes take at peak HBM
+    # bandwidth; the larger term binds.
+    top_weights = sum(e[3].n * e[3].k for e in top.entries)
+    gamma = 32 * CU_COUNT * CLOCK_HZ * per_launch_us * 1e-6 / top_weights
+    hbm_term = 32 * alg_bytes / top_weights / (HBM_PEAK_GBS * 1e9 / (CU_COUNT * CLOCK_HZ))
     ms = res[(N.FMT_BITCOS, "bf16")]
     value = payload[N.FMT_BITCOS] / (ms * 1e-3) / 1e9
     out = {
@@ -598,6 +651,8 @@ def main():
             "gemvs_per_step": len(packed[N.FMT_BITCOS]),
             "weights_per_step": weights,
             "payload_bytes_per_step": int(payload[N.FMT_BITCOS]),
+            "total_bytes_per_step": int(sum(e[3].total_bytes + m * (e[3].k * 2 + e[3].n * 4)
+                                            for e in packed[N.FMT_BITCOS])),
             "device_copies": copies,
         },
         "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
@@ -640,7 +695,10 @@ def main():
         "kernel": f"{kname}<{top.tile[0]},{top.tile[1]},bf16,table>: {len(top.entries)} GEMVs in one launch",
         "per_launch_us": round(per_launch_us, 3),
         "bytes_per_launch": int(alg_bytes),
+        "two_term": {"cu_cycles_per_32w": round(gamma, 4), "hbm_cu_cycles_per_32w": round(hbm_term, 4),
+                     "binds": "instructions" if gamma > hbm_term else "hbm"},
     }
+    out["sclk_mhz_under_load"] = sclk
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wk)
     print(json.dumps(out))
