@@ -278,8 +278,12 @@ typedef struct bitcos_launch_info {
   int32_t seg_lanes;       /* lanes that share one row (power of two)          */
   int32_t rows_per_step;   /* rows a wave covers per step = 64 / seg_lanes      */
   int32_t lanes_used;      /* lanes per row that hold weights                   */
-  int64_t waves;           /* waves launched                                   */
-  int64_t workgroups;      /* workgroups launched (256 threads each)           */
+  int64_t waves;           /* work units (rows_per_step rows each); a persistent
+                              launch runs at most the resident waves, each
+                              taking a share of the units                      */
+  int64_t workgroups;      /* waves / 4, rounded up (a nominal 256-thread
+                              grouping; the kernels' own workgroups hold 8 to
+                              16 waves)                                        */
   int32_t kernel;          /* BITCOS_KERNEL_*                                   */
   int32_t reserved;
 } bitcos_launch_info;

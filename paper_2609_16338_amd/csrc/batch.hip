@@ -242,7 +242,7 @@ int bitcos_describe(const bitcos_layout* L, int32_t m, int32_t x_dtype, bitcos_l
     out->rows_per_step = bitcos::kMfmaUnitRows;
     out->lanes_used = 4;
     out->waves = units;
-    out->workgroups = (units + 7) / 8;
+    out->workgroups = (units + 3) / 4;
     out->kernel = BITCOS_KERNEL_SMALL_BATCH;
     out->reserved = 0;
     return BITCOS_OK;

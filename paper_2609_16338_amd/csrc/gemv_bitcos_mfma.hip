@@ -25,7 +25,7 @@ int launch_bitcos_mfma(const BatchHeader& h, const GemvDesc* table_dev, const Ge
   a.count = h.count;
   a.pad = 0;
   a.one = one;
-  const int threads = bitcos_k::kMfmaThreads;
+  const int threads = bitcos_k::mfma_threads(bf16, h.any_xscale != 0);
   const int64_t blocks = persistent_blocks(reinterpret_cast<const void*>(fn), h.total_units, threads);
   if (blocks <= 0 || blocks > 0x7FFFFFFF) return BITCOS_E_HIP;
   hipLaunchKernelGGL(fn, dim3(static_cast<unsigned>(blocks)), dim3(threads), 0,
