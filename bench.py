@@ -623,7 +623,7 @@ def main():
     # clock): its measured time against the time its bytes take at peak HBM
     # bandwidth; the larger term binds.
     top_weights = sum(e[3].n * e[3].k for e in top.entries)
-    gamma = 32 * CU_COUNT * CLOCK_HZ * per_launch_us * 1e-6 / top_weights
+    launch_gamma = 32 * CU_COUNT * CLOCK_HZ * per_launch_us * 1e-6 / top_weights
     hbm_term = 32 * alg_bytes / top_weights / (HBM_PEAK_GBS * 1e9 / (CU_COUNT * CLOCK_HZ))
     ms = res[(N.FMT_BITCOS, "bf16")]
     value = payload[N.FMT_BITCOS] / (ms * 1e-3) / 1e9
@@ -695,8 +695,8 @@ def main():
         "kernel": f"{kname}<{top.tile[0]},{top.tile[1]},bf16,table>: {len(top.entries)} GEMVs in one launch",
         "per_launch_us": round(per_launch_us, 3),
         "bytes_per_launch": int(alg_bytes),
-        "two_term": {"cu_cycles_per_32w": round(gamma, 4), "hbm_cu_cycles_per_32w": round(hbm_term, 4),
-                     "binds": "instructions" if gamma > hbm_term else "hbm"},
+        "two_term": {"cu_cycles_per_32w": round(launch_gamma, 4), "hbm_cu_cycles_per_32w": round(hbm_term, 4),
+                     "binds": "instructions" if launch_gamma > hbm_term else "hbm"},
     }
     out["sclk_mhz_under_load"] = sclk
     if not args.no_cpu_baseline:

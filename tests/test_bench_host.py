@@ -90,3 +90,12 @@ def test_supported_reports_baselines_without_a_long_row_kernel():
         assert bench.supported(entries, "bf16", 1) is bf16_ok
         assert bench.supported(entries, "int8", 1)
         assert bench.supported(entries, "bf16", 4) is bf16_ok  # baselines at m > 1: batch-1 launches
+
+
+def test_main_shadows_no_module_function():
+    """A local of main() named like a module-level function (say `gamma`)
+    would make main's call of that function fail before the function runs."""
+    import inspect
+    funcs = {n for n, v in vars(bench).items() if inspect.isfunction(v)}
+    for fn in (bench.main,):
+        assert not (set(fn.__code__.co_varnames) & funcs), set(fn.__code__.co_varnames) & funcs
