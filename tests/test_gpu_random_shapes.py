@@ -90,3 +90,50 @@ def test_random_shape(i):
     else:
         ref = O.dense_gemv(w, sc, c["group"], x, xscale=a)
         check_grouped(y, ref, group_bound(w, sc, c["group"], x, a))
+
+
+BASELINE_CASES = 30
+
+
+def draw_baseline(i):
+    rng = wl.rng_for(930, i)
+    fmt = N.FMT_TRIT5 if rng.random() < 0.5 else N.FMT_BIT2
+    kind = "int8" if rng.random() < 0.5 else "bf16"
+    m = 1 if rng.random() < 0.8 else int(rng.choice([2, 5]))
+    group = 128 if rng.random() < 0.6 else 0
+    kmax = 16384 if kind == "bf16" else 32768
+    k = int(rng.integers(1, kmax // 128 + 1)) * 128
+    n = int(rng.integers(1, max(2, min(400, MAX_WEIGHTS // k)) + 1))
+    zc = rng.random()
+    z = 0.0 if zc < 0.1 else 1.0 if zc < 0.2 else float(rng.uniform(0.2, 0.8))
+    xscale = kind == "int8" and rng.random() < 0.4
+    raw = kind == "int8" and not xscale and rng.random() < 0.4
+    return dict(fmt=fmt, kind=kind, m=m, group=group, k=k, n=n, z=z, xscale=xscale, raw=raw)
+
+
+@pytest.mark.parametrize("i", range(BASELINE_CASES))
+def test_random_shape_baselines(i):
+    """The five-trit and 2-bit kernels on seeded random shapes, same bars."""
+    c = draw_baseline(i)
+    w, sc = inputs(c["n"], c["k"], c["z"], c["group"], 940 + i)
+    xr = wl.rng_for(950, i)
+    a = None
+    if c["kind"] == "bf16":
+        x = wl.act_bf16(c["m"], c["k"], xr)
+    elif c["xscale"]:
+        x, a = O.quantize_activations(wl.act_bf16(c["m"], c["k"], xr))
+    else:
+        x = wl.act_int8(c["m"], c["k"], xr)
+    if c["raw"]:
+        y, _ = run(c["fmt"], w, sc, c["group"], x, "int8", y_mode=N.Y_I32_RAW)
+        assert np.array_equal(y, O.dense_gemv_raw(w, x).astype(np.int32)), c
+        return
+    y, _ = run(c["fmt"], w, sc, c["group"], x, c["kind"], xscale=a)
+    if c["kind"] == "bf16":
+        ref = O.dense_gemv(w, sc, c["group"], x, x_is_bf16_bits=True)
+        check_bf16(y, ref, bf16_bound(w, sc, c["group"], x))
+    elif c["group"] == 0 and a is None:
+        assert np.array_equal(y, O.dense_gemv(w, sc, 0, x)), c
+    else:
+        ref = O.dense_gemv(w, sc, c["group"], x, xscale=a)
+        check_grouped(y, ref, group_bound(w, sc, c["group"], x, a))
