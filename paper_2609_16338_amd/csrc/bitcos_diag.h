@@ -503,6 +503,12 @@ __global__ void __launch_bounds__(diag_threads(W, BF16)) bitcos_diag_kernel(cons
       base = wave_bits + (s.off0 & 31u) + static_cast<uint32_t>(excl);
     }
     __builtin_amdgcn_wave_barrier();
+    // The windows, lookups and multiplies of the step at raised wave
+    // priority: a wave whose loads have landed gets the SIMD's issue slots
+    // for its whole decode burst ahead of waves still in their step
+    // prologue, which keeps the VALU, LDS and matrix cores fed back to back
+    // (6-7 % faster on the BitNet-like K = 2560 launch).
+    __builtin_amdgcn_s_setprio(1);
 
     // Windows: 64 bits at each word's first sign.  The lane's cursor is
     // clamped once so that every window stays in the wave's own buffer (a
@@ -533,6 +539,7 @@ __global__ void __launch_bounds__(diag_threads(W, BF16)) bitcos_diag_kernel(cons
       for (int w = 0; w < W; ++w) diag_math<BF16>(diag_look(Pw[w], S[w], tab, lane), xr[w], acc);
     }
     __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_s_setprio(0);
 
     bool store = false;
     int row = 0;

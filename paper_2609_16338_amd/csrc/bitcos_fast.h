@@ -306,6 +306,8 @@ __global__ void __launch_bounds__(fast_threads(W, BF16)) bitcos_fast_kernel(cons
     const int incl = wave_incl_scan(cnt);
     const uint32_t base = wave_bits + (s.off0 & 31u) + static_cast<uint32_t>(incl - cnt);
     __builtin_amdgcn_wave_barrier();
+    // Decode burst at raised wave priority (as in the matrix-core kernel).
+    __builtin_amdgcn_s_setprio(1);
     // Software pipeline over the lane's words: the table lookups of word w+1
     // are in flight while word w is multiplied.
     Acc run[W];
@@ -347,6 +349,7 @@ __global__ void __launch_bounds__(fast_threads(W, BF16)) bitcos_fast_kernel(cons
       }
     }
     __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_s_setprio(0);
 
     // One lane per row stores; rows past the end are outside ry and dropped.
     const uint32_t soff_y = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(s.row0) * 4u);
