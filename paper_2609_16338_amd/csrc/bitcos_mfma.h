@@ -312,6 +312,9 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
     }
     __builtin_amdgcn_wave_barrier();
 
+    // The groups at raised wave priority (as in the batch-1 kernels): int8
+    // 9 % faster at M = 4 on the Qwen3-32B-like layers, bf16 1.5 %.
+    __builtin_amdgcn_s_setprio(1);
     // Groups: the MFMAs of group q, then the epilogue of group q - 1 (whose
     // MFMAs have had a group's worth of work to finish).
     CV cg[2][RT];
@@ -387,6 +390,7 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
       for (int i = 0; i < 4; ++i) xa_prev[i] = xa_q[i];
     }
     epilogue(3, cg[1], xa_prev);
+    __builtin_amdgcn_s_setprio(0);
     __builtin_amdgcn_wave_barrier();
 
     if (cs.last) {  // store the unit: y[m][row]; rows past n and batch rows past M are dropped
