@@ -274,9 +274,6 @@ __global__ void __launch_bounds__(kBlock) trit5_gemv_kernel(const KernelArgs a) 
     uint16_t SC0[BK];
 #pragma unroll
     for (int t = 0; t < BK; ++t) SC0[t] = SC1[t];
-    s1 = gen.next(a);
-    if (s1.valid) load_c(s1, cw1, o1, SC1);
-
     if (s0.di != xdi) {
       xdi = s0.di;
       const auto& g = desc_at<TABLE>(a, xdi);
@@ -292,12 +289,19 @@ __global__ void __launch_bounds__(kBlock) trit5_gemv_kernel(const KernelArgs a) 
       tensor_scale = half_bits_to_float(gp_u16(g.scales)[0]);
       mode = g.mode;
       ydst = g.y;
+      wait_vmem_all();
     }
+    // The next step's loads, issued after the activations of a GEMV the wave
+    // enters have been waited for, so that no wait inside the step covers them.
+    s1 = gen.next(a);
+    if (s1.valid) load_c(s1, cw1, o1, SC1);
 
     const int row = s0.row0 + rho;
     const bool live = row < s0.row_end;
     Acc run[BK];
     Acc acc = Acc(0);
+    // The decode burst at raised wave priority, as in the BITCOS kernels.
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int t = 0; t < BK; ++t) {
       const uint32_t* x = xr[t];
@@ -332,6 +336,7 @@ __global__ void __launch_bounds__(kBlock) trit5_gemv_kernel(const KernelArgs a) 
       }
       run[t] = acc;
     }
+    __builtin_amdgcn_s_setprio(0);
     finish_row<SEG, BF16, BK, 1>(mode, ydst, run, row, live, j, 0, xs, SC0, tensor_scale);
   }
 }
@@ -417,9 +422,6 @@ __global__ void __launch_bounds__(kBlock) bit2_gemv_kernel(const KernelArgs a) {
     for (int w = 0; w < WB; ++w) cw0[w] = cw1[w];
 #pragma unroll
     for (int q = 0; q < NQ; ++q) SC0[q] = SC1[q];
-    s1 = gen.next(a);
-    if (s1.valid) load_c(s1, cw1, SC1);
-
     if (s0.di != xdi) {
       xdi = s0.di;
       const auto& g = desc_at<TABLE>(a, xdi);
@@ -452,12 +454,19 @@ __global__ void __launch_bounds__(kBlock) bit2_gemv_kernel(const KernelArgs a) {
       tensor_scale = half_bits_to_float(gp_u16(g.scales)[0]);
       mode = g.mode;
       ydst = g.y;
+      wait_vmem_all();
     }
+    // The next step's loads, issued after the activations of a GEMV the wave
+    // enters have been waited for, so that no wait inside the step covers them.
+    s1 = gen.next(a);
+    if (s1.valid) load_c(s1, cw1, SC1);
 
     const int row = s0.row0 + rho;
     const bool live = row < s0.row_end;
     Acc run[WB];
     Acc acc = Acc(0);
+    // The decode burst at raised wave priority, as in the BITCOS kernels.
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int w = 0; w < WB; ++w) {
       const uint32_t c = cw0[w];
@@ -477,6 +486,7 @@ __global__ void __launch_bounds__(kBlock) bit2_gemv_kernel(const KernelArgs a) {
       }
       run[w] = acc;
     }
+    __builtin_amdgcn_s_setprio(0);
     finish_row<SEG, BF16, WB, 8>(mode, ydst, run, row, live, j, ph, xs, SC0, tensor_scale);
   }
 }
