@@ -60,11 +60,25 @@ inline bool choose_tile(int units_per_row, int max_per_lane, Tile* t, bool wide 
 // which the step's fixed work (prefix of the row's counts, sign offsets,
 // row sums) is spread; at K = 4096 eight words per lane on 16-lane rows run
 // the Qwen3-8B-like set 16 % (int8) and 8 % (bf16) faster than two words on
-// 64-lane rows, and sixteen words per lane are slower again.  Longer rows
-// (int8 K > 16384) take up to 16 words.
+// 64-lane rows, and sixteen words per lane are slower again.  bf16 takes the
+// widest of those tiles with at most 5 words per lane when there is one
+// (its kernels then run 3 waves per SIMD instead of 2): 4 words on 32-lane
+// rows at K = 4096 and on 64-lane rows at K = 8192 measured 4-6 % faster
+// than 8 words.  Longer rows (int8 K > 16384) take up to 16 words.
 inline bool bitcos_tile(int k, bool bf16, Tile* t) {
   constexpr int kWideWords = 8;
-  return choose_tile(k / 32, kWideWords, t, true) || choose_tile(k / 32, bf16 ? kMaxWordsBf16 : kMaxWordsI8, t);
+  constexpr int kWordsAt3Waves = 5;  // bf16: most words per lane at 3 waves per SIMD
+  Tile wide;
+  if (!choose_tile(k / 32, kWideWords, &wide, true))
+    return choose_tile(k / 32, bf16 ? kMaxWordsBf16 : kMaxWordsI8, t);
+  Tile narrow;
+  const auto idle_free = [&](const Tile& x) { return double(k / 32) / double(x.seg * x.per_lane); };
+  if (bf16 && choose_tile(k / 32, kWordsAt3Waves, &narrow, true) && idle_free(narrow) > idle_free(wide) - 1e-12) {
+    *t = narrow;
+    return true;
+  }
+  *t = wide;
+  return true;
 }
 
 // Default rows per sign offset: one, so every kernel (any rows per wave step,

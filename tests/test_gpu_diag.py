@@ -33,7 +33,9 @@ def _need_gpu():
 # K -> (words per lane, lanes per row): 96 -> (1, 4) ragged, 128 -> (1, 4),
 # 256 -> (2, 4), 512 -> (4, 4), 1024 -> (8, 4), 2048 -> (8, 8),
 # 2400 -> (5, 16) ragged, 2560 -> (5, 16), 4096 -> (8, 16), 5120 -> (5, 32),
-# 6912 -> (7, 32) ragged, 8192 -> (8, 32), 12288 -> (6, 64), 16384 -> (8, 64).
+# 6912 -> (7, 32) ragged, 8192 -> (8, 32), 12288 -> (6, 64), 16384 -> (8, 64)
+# (int8; bf16 takes at most 5 words where an equally full tile allows it:
+# 1024 -> (4, 8), 2048 -> (4, 16), 4096 -> (4, 32), 8192 -> (4, 64)).
 KS = [96, 128, 256, 512, 1024, 2048, 2400, 2560, 4096, 5120, 6912, 8192, 12288, 16384]
 
 

@@ -37,7 +37,8 @@ def _need_gpu():
 
 # K -> (words per lane, lanes per row): 128 (1, 4), 256 (2, 4), 384 (3, 4),
 # 640 (5, 4), 1024 (8, 4), 1152 (5, 8) ragged, 2048 (8, 8), 2560 (5, 16),
-# 4096 (8, 16), 5120 (5, 32), 6912 (7, 32) ragged, 8192 (8, 32), 12288 (6, 64).
+# 4096 (8, 16), 5120 (5, 32), 6912 (7, 32) ragged, 8192 (8, 32), 12288 (6, 64)
+# (int8; bf16: 1024 (4, 8), 2048 (4, 16), 4096 (4, 32), 8192 (4, 64)).
 KS = [128, 256, 384, 640, 1024, 1152, 2048, 2560, 4096, 5120, 6912, 8192, 12288]
 
 

@@ -222,6 +222,12 @@ def test_describe_tiles():
         assert (info.per_lane, info.seg_lanes) == (per_lane, seg), k
         assert info.rows_per_step * info.seg_lanes == 64
         assert info.lanes_used * info.per_lane >= k // 32
+    # bf16: the widest equally full tile with at most 5 words per lane, if any
+    for k, per_lane, seg in [(2560, 5, 16), (4096, 4, 32), (8192, 4, 64), (6912, 7, 32), (12288, 6, 64),
+                             (1024, 4, 8)]:
+        L = api.bitcos_plan(np.zeros((8, k), np.int8), 128, 0)
+        info = api.describe(L, 1, N.X_BF16)
+        assert (info.per_lane, info.seg_lanes) == (per_lane, seg), k
 
 
 def test_describe_kernel_choice():
