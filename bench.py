@@ -2,36 +2,47 @@
 """Benchmark: BITCOS ternary GEMV effective weight bandwidth on one MI355X.
 
 A step is one batch-1 pass over a whole decode layer set (every GEMV of every
-layer, inputs already resident in HBM), replayed from a HIP graph: W untimed
-replays, then K timed ones, after a one-off 100 ms untimed warm-up that lifts
-the GPU out of the idle clocks of the host-side packing.  Two device copies of
-the set are replayed in turn, so a weight is re-read only after 2 x 411 MB of
-other payload, more than twice the 256 MB Infinity Cache.  The
-headline is the BitNet-2B-like set: 30 layers x {q, o 2560x2560; k, v
-640x2560; gate, up 6912x2560; down 2560x6912}, z = 0.42 iid, one fp16 scale
-per tensor, bf16 activations ~ N(0, 1) (the int8-quantised variant is reported
-beside it).  value = sum of BITCOS payload bytes (bitmap + signs + scales) /
-step time.  The same step over the five-trit and 2-bit layouts of the same
-weights gives the same-GPU speedups.
+layer, inputs already resident in HBM), replayed from a HIP graph.  The
+headline (N = 1) is the largest layer set that fits one GPU, the
+Qwen3-32B-like set: 64 layers x {q, o 5120x5120; k, v 1024x5120; gate, up
+25600x5120; down 5120x25600}, per-row zero density drawn uniform in
+[0.30, 0.60], group-128 fp16 scales, bf16 activations ~ N(0, 1); the same
+step with int8 activations (quantised per group of 128 by the library) is
+reported beside it.  value = sum of BITCOS payload bytes (bitmap + signs +
+scales) / step time.  The same step over the five-trit and 2-bit layouts of
+the same weights gives the same-GPU speedups.  The BitNet-2B-like set is
+timed the same way and reported as an extra block.
 
---workload and --batch M select the other layer sets and M activation rows
-per GEMV (BITCOS runs M > 1 in one launch per tile on its small-batch
-kernel; the five-trit and 2-bit layouts have no such kernel and take M
-batch-1 launches, as their entry points do).  A baseline with no kernel for
-a set (bf16 activations on rows longer than 16384) is reported as null.
+Timing: every (format, activation type) gets its own untimed warm-up of at
+least --warm-ms milliseconds of replays (the GPU's clocks ramp for ~30 ms
+after an idle stretch such as host-side packing or a graph capture), then
+--warmup more untimed replays, then --steps timed ones bracketed by events
+on the replay stream.  Two device copies of the set are replayed in turn, so
+a weight is re-read only after more than twice the 256 MB Infinity Cache of
+other payload has streamed by.
 
-Prints ONE JSON line.  roofline: the dominant launch (the K = 2560 GEMVs of
-the step, one persistent launch) timed alone, from a graph of ten back-to-back
-launches; achieved = its
-algorithmic bytes (payload + 2 K activation bytes + 4 N output bytes per GEMV)
-per launch time, against the 8 TB/s HBM peak; traffic = its measured HBM
-bytes (FETCH_SIZE + WRITE_SIZE scaled by a plain copy's counters, stored under
-profiles/) while the kernel sources are unchanged; two_term: the launch's
-time and its bytes at peak HBM bandwidth, both in CU-cycles per 32 weights
-at the nominal 2.4 GHz, and which is larger.  sclk_mhz_under_load: the
-shader clock rocm-smi reads while that launch replays (untimed, after the
-timed runs).  cpu_baseline: the oracle's decode + dense GEMV on whole
-layer-0 matrices on the host, about 12 s of work.
+Self-check: after timing, the outputs of the last replay of every device
+copy are compared, on sampled rows of every GEMV, with the dense definition
+y = sum_g S a sum_k W x computed here in float64 from the same weights and
+activations (bars: bf16 activations |y - ref| <= 1e-3 sum_k |S W x|; int8
+activations with activation scales |y - ref| <= 1e-5 sum_g |S a A|).  A
+mismatch prints an error line and exits with status 3 instead of a value.
+
+Prints ONE JSON line.  roofline: the dominant launch (the persistent launch
+carrying most of the step's bytes) timed alone from a graph of ten
+back-to-back launches; achieved = its algorithmic bytes (payload + M K
+activation bytes + 4 M N output bytes per GEMV) per launch time, against the
+8 TB/s HBM peak; traffic = its measured HBM bytes (FETCH_SIZE + WRITE_SIZE
+scaled by a plain copy's counters, stored under profiles/) while the kernel
+sources are unchanged; two_term: the launch's time and its bytes at peak HBM
+bandwidth in CU-cycles per 32 weights at the nominal 2.4 GHz, and which
+term is larger.  cpu_baseline: the oracle's decode + dense GEMV on whole
+layer-0 matrices on the host (about 12 s of work).
+
+Other modes print their own JSON line: --sweep (zero-density sweep on one
+8192 x 8192 matrix), --gamma (two-term roofline on cache-resident data),
+--hbm-read (plain streaming-read bandwidth of this GPU), --profile-pass (the
+dominant launch and a calibration copy, for counter runs).
 """
 
 from __future__ import annotations
@@ -51,40 +62,63 @@ sys.path.insert(0, ROOT)
 import workloads as wl  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
+CU_COUNT = 256
+CLOCK_HZ = 2.4e9
 FMT_NAMES = {1: "bitcos", 2: "trit5", 3: "bit2"}
 METRIC = "ternary GEMV effective weight GB/s (% of 8 TB/s HBM peak); speedup vs 5-trit"
+HEADLINE = "qwen3_32b_layers"
+SAMPLE_ROWS = 6  # rows of every GEMV checked after timing (first, last and random ones)
 
 
-def parse():
+def parse(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=200)
-    ap.add_argument("--workload", default="bitnet2b_layers")
+    ap.add_argument("--warm-ms", type=float, default=200.0,
+                    help="untimed replays for at least this long before each format's timed window")
+    ap.add_argument("--workload", default=HEADLINE)
+    ap.add_argument("--extra", default="bitnet2b_layers",
+                    help="comma-separated layer sets timed after the headline and reported as extra blocks")
     ap.add_argument("--batch", type=int, default=1,
                     help="activation rows per GEMV (1..16); BITCOS runs M > 1 on its small-batch kernel")
     ap.add_argument("--layers", type=int, default=0, help="0 = the workload's layer count")
     ap.add_argument("--copies", type=int, default=2,
-                    help="device copies of the layer set, replayed in turn (2 x 411 MB > 2 x the 256 MB Infinity Cache)")
+                    help="device copies of the layer set, replayed in turn (more than 2 x the 256 MB Infinity Cache)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-baselines", action="store_true", help="skip the five-trit / 2-bit steps")
+    ap.add_argument("--no-check", action="store_true", help="skip the output self-check after timing")
     ap.add_argument("--threads", type=int, default=min(16, os.cpu_count() or 1))
+    ap.add_argument("--out", default="", help="also write the JSON line to this file")
     ap.add_argument("--profile-pass", action="store_true",
                     help="for counter runs: the dominant BITCOS launch x5, then a plain 256 MiB device copy x5")
     ap.add_argument("--sweep", action="store_true",
                     help="zero-density sweep on one 8192 x 8192 matrix: BITCOS vs five-trit vs 2-bit (own JSON line)")
     ap.add_argument("--gamma", action="store_true",
                     help="two-term roofline: cycles per 32 weights on cache-resident data vs z (own JSON line)")
+    ap.add_argument("--hbm-read", action="store_true",
+                    help="plain streaming-read bandwidth of this GPU (own JSON line)")
     ap.add_argument("--sweep-copies", type=int, default=40,
                     help="device copies of each swept matrix streamed per launch (> 2 x the 256 MB Infinity Cache)")
-    return ap.parse_args()
+    return ap.parse_args(argv)
 
 
-# Sources of the streaming BITCOS kernel: a stored HBM-traffic measurement is
-# reported only while these files are unchanged.
-KERNEL_SOURCES = ["bitcos_diag.h", "bitcos_fast.h", "bitcos_kernel.h", "mfma_common.h", "device_common.h", "batch.h",
-                  "batch.hip", "gemv_bitcos.hip", "gemv_bitcos_d16.hip", "launch_common.h", "plan.h"]
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "bitcos_diag_bf16_bitnet2b_k2560_traffic.txt")
+def emit(obj, args):
+    line = json.dumps(obj)
+    print(line, flush=True)
+    if getattr(args, "out", ""):
+        with open(args.out, "w") as f:
+            f.write(line + "\n")
+
+
+# Sources of the BITCOS kernels: a stored HBM-traffic measurement is reported
+# only while these files are unchanged.
+KERNEL_SOURCES = ["bitcos_diag.h", "bitcos_fast.h", "bitcos_kernel.h", "bitcos_mfma.h", "mfma_common.h",
+                  "device_common.h", "batch.h", "batch.hip", "gemv_bitcos.hip", "launch_common.h", "plan.h"]
+TRAFFIC_FILES = {
+    "qwen3_32b_layers": os.path.join(ROOT, "profiles", "bitcos_fast_bf16_qwen3_32b_k5120_traffic.txt"),
+    "bitnet2b_layers": os.path.join(ROOT, "profiles", "bitcos_diag_bf16_bitnet2b_k2560_traffic.txt"),
+}
 COPY_MIB = 256
 
 
@@ -97,13 +131,14 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def stored_traffic():
+def stored_traffic(workload):
     """HBM bytes per launch of the dominant kernel from the FETCH_SIZE / WRITE_SIZE
     passes (scaled by the copy calibration), or None if the kernel changed since."""
+    path = TRAFFIC_FILES.get(workload)
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(path) as f:
             kv = dict(line.split(":", 1) for line in f if ":" in line and not line.startswith("#"))
-    except OSError:
+    except (OSError, TypeError):
         return None
     kv = {k.strip(): v.strip() for k, v in kv.items()}
     if kv.get("kernel_source_hash") != kernel_source_hash():
@@ -114,8 +149,21 @@ def stored_traffic():
         return None
 
 
-def build_set(wk, layers, fmts, threads):
-    """Pack every matrix of the layer set in every format (host), upload to HBM."""
+# ---------------------------------------------------------------------------
+# Inputs
+# ---------------------------------------------------------------------------
+
+def sample_rows(n, l, mi, count=SAMPLE_ROWS):
+    rng = np.random.default_rng([l, mi, n])
+    rows = {0, n - 1} | set(rng.choice(n, size=min(max(count - 2, 0), n), replace=False).tolist())
+    return np.array(sorted(rows))
+
+
+def build_set(wk, layers, fmts, threads, samples=None):
+    """Pack every matrix of the layer set in every format (host), upload to HBM.
+
+    With `samples` (a dict), the weights and scales of a few rows of every
+    matrix are kept there, keyed by (layer, matrix), for the self-check."""
     import torch
 
     from paper_2609_16338_amd import api
@@ -127,37 +175,51 @@ def build_set(wk, layers, fmts, threads):
         w, sc = wl.matrix_inputs(wk.cid, l, mi, spec)
         out = {}
         for fmt in fmts:
-            L, blob = api.plan_and_pack(fmt, w, sc, spec.group)
-            out[fmt] = (L, blob)
-        return job, out
+            out[fmt] = api.plan_and_pack(fmt, w, sc, spec.group)
+        keep = None
+        if samples is not None:  # (rows, their weights, their fp16 scale bits [rows][k/128] or [1][1])
+            rows = sample_rows(spec.n, l, mi)
+            sbits = sc.reshape(spec.n, spec.k // 128)[rows] if spec.group == 128 else sc.reshape(1, 1)
+            keep = (rows, np.ascontiguousarray(w[rows]), np.ascontiguousarray(sbits))
+        return job, out, keep
 
     packed = {}
     with cf.ThreadPoolExecutor(max_workers=threads) as ex:
-        for (l, mi, spec), out in ex.map(one, jobs):
+        for (l, mi, spec), out, keep in ex.map(one, jobs):
             for fmt, (L, blob) in out.items():
                 packed.setdefault(fmt, []).append((l, mi, spec, L, torch.from_numpy(blob).cuda()))
+            if keep is not None:
+                samples[(l, mi)] = keep
     return packed
+
+
+def bf16_bits_to_f64(bits):
+    return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
 
 
 def activations(wk, kinds, m=1):
     """Per distinct K: device activations [m, k] (bf16, and int8 + per-group
-    scales via the library)."""
+    scales via the library), and host float64 copies of what the GEMVs read."""
     import torch
 
     from paper_2609_16338_amd import api
 
-    acts = {}
+    acts, host = {}, {}
     for k in sorted({s.k for s in wk.matrices}):
         xb = wl.activation_inputs(wk.cid, "bf16", m, k)
         xbd = torch.from_numpy(xb.view(np.int16)).view(torch.bfloat16).cuda()
         acts[("bf16", k)] = (xbd, None)
+        host[("bf16", k)] = (bf16_bits_to_f64(xb).reshape(m, k), None)
         if "int8" in kinds:
             q = torch.empty((m, k), dtype=torch.int8, device="cuda")
             a = torch.empty((m, k // 128), dtype=torch.float32, device="cuda")
             api.quantize_activations(xbd, q, a)
             acts[("int8", k)] = (q, a)
     torch.cuda.synchronize()
-    return acts
+    for (kind, k), (x, a) in acts.items():
+        if kind == "int8":  # the GEMV's own inputs, as the library quantised them
+            host[(kind, k)] = (x.cpu().numpy().astype(np.float64), a.cpu().numpy().astype(np.float64))
+    return acts, host
 
 
 def supported(entries, kind, m=1):
@@ -207,6 +269,7 @@ def make_batches(entries, acts, kind):
             b = api.Batch([e[3] for e in ents], [e[4] for e in ents], xs, [y[r0:r1].reshape(-1) for y in ys],
                           xss if any(v is not None for v in xss) else None)
             b.tile = tile[1:]
+            b.kernel = tile[0]
             b.entries = ents
             b.outputs = ys
             batches.append(b)
@@ -219,8 +282,13 @@ def make_step(entries, acts, kind):
     def step():
         for b in batches:
             b.run()
+    step.batches = batches
     return step, batches
 
+
+# ---------------------------------------------------------------------------
+# Graphs and timing
+# ---------------------------------------------------------------------------
 
 def capture(step):
     """A graph of one call of `step`, holding `step` (and through it the batch
@@ -240,40 +308,46 @@ def capture(step):
     return g
 
 
-def time_graph(g, steps, warmup):
+def warm(graphs, min_ms):
+    """Replay the graphs in turn for at least `min_ms` of wall time, untimed.
+
+    After an idle stretch (host-side packing, graph capture, another
+    format's checks) the GPU's clocks start low and the first ~150 replays
+    of a step run up to 20% slower than the steady state a decode loop
+    sees; every timed window is preceded by this."""
     import torch
-    for _ in range(warmup):
-        g.replay()
-    torch.cuda.synchronize()
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
-    start.record()
-    for _ in range(steps):
-        g.replay()
-    end.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    return start.elapsed_time(end) / steps, wall
+    n = 0
+    while (time.perf_counter() - t0) * 1e3 < min_ms:
+        for _ in range(10):
+            graphs[n % len(graphs)].replay()
+            n += 1
+        torch.cuda.synchronize()
+    return n, (time.perf_counter() - t0) * 1e3
 
 
-def time_graphs(graphs, steps, warmup):
-    """time_graph over several graphs replayed in turn (one replay = one step)."""
+def time_graphs(graphs, steps, warmup, warm_ms=0.0):
+    """Per-replay time (ms) of the graphs replayed in turn, one replay = one
+    step: a time-based warm-up, `warmup` more replays, then `steps` timed."""
     import torch
+    if warm_ms > 0:
+        warm(graphs, warm_ms)
     n = len(graphs)
     for i in range(warmup):
         graphs[i % n].replay()
     torch.cuda.synchronize()
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
-    t0 = time.perf_counter()
     start.record()
     for i in range(steps):
         graphs[i % n].replay()
     end.record()
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    return start.elapsed_time(end) / steps, wall
+    return start.elapsed_time(end) / steps
+
+
+def time_graph(g, steps, warmup, warm_ms=0.0):
+    return time_graphs([g], steps, warmup, warm_ms)
 
 
 def device_copies(entries, copies):
@@ -282,24 +356,6 @@ def device_copies(entries, copies):
     for _ in range(copies - 1):
         sets.append([(l, mi, spec, L, blob.clone()) for (l, mi, spec, L, blob) in entries])
     return sets
-
-
-def warm_device(g, min_ms=100.0):
-    """Replay a graph for at least `min_ms` of wall time, untimed.
-
-    After the host-side packing the GPU has idled and its clocks start low:
-    the first ~150 replays of the BitNet-like step run up to 20% slower than
-    the steady state a decode loop sees.  This brings the device to that
-    state once, before anything is timed."""
-    import torch
-    t0 = time.perf_counter()
-    n = 0
-    while (time.perf_counter() - t0) * 1e3 < min_ms:
-        for _ in range(20):
-            g.replay()
-        n += 20
-        torch.cuda.synchronize()
-    return n, (time.perf_counter() - t0) * 1e3
 
 
 def gpu_clock_under_load(g, seconds=1.5):
@@ -330,6 +386,227 @@ def gpu_clock_under_load(g, seconds=1.5):
         res = None
     torch.cuda.synchronize()
     return res
+
+
+# ---------------------------------------------------------------------------
+# Self-check of the timed outputs
+# ---------------------------------------------------------------------------
+
+def dense_rows(w_rows, s_bits, group, x, xscale):
+    """y[m, r] and its error scales for the sampled rows, from the definition
+    y = sum_g S[r, g] a[m, g] sum_{k in g} W[r, k] x[m, k] in float64 (S from
+    the fp16 bits s_bits: [r][k/128], or [1][1] for one scale per tensor).
+
+    Returns (y, sum_k |S W x| (bf16 bar), sum_g |S a A| (int8 bar))."""
+    r, k = w_rows.shape
+    m = x.shape[0]
+    wf = w_rows.astype(np.float64)
+    s_rows = np.asarray(s_bits, dtype=np.uint16).view(np.float16).astype(np.float64)
+    if group == 128 or xscale is not None:
+        g = k // 128
+        A = np.einsum("rgk,mgk->mrg", wf.reshape(r, g, 128), x.reshape(m, g, 128))
+        S = s_rows if s_rows.shape[1] == g else np.full((r, g), s_rows[0, 0])
+        a = np.ones((m, 1, g)) if xscale is None else xscale.reshape(m, 1, g)
+        terms = S[None] * a * A
+        y = terms.sum(axis=2)
+        gbar = np.abs(terms).sum(axis=2)
+        Sk = np.repeat(S, 128, axis=1)
+        ak = np.ones((m, k)) if xscale is None else np.repeat(xscale.reshape(m, g), 128, axis=1)
+        kbar = (np.abs(ak * x)) @ np.abs(Sk * wf).T
+    else:
+        s = s_rows[0, 0]
+        y = s * (x @ wf.T)
+        kbar = s * (np.abs(x) @ np.abs(wf).T)
+        gbar = np.abs(y)
+    return y, kbar, gbar
+
+
+def check_outputs(batches, samples, xhost, kind):
+    """Compare the outputs of the last replay with dense_rows on the sampled
+    rows of every GEMV.  Returns (ok, rows checked, worst error / allowed)."""
+    import torch
+    torch.cuda.synchronize()
+    ok, rows_checked, worst = True, 0, 0.0
+    for b in batches:
+        for e, y in zip(b.entries, b.outputs):
+            l, mi, spec = e[0], e[1], e[2]
+            rows, w_rows, s_rows = samples[(l, mi)]
+            x, xs = xhost[(kind, spec.k)]
+            ref, kbar, gbar = dense_rows(w_rows, s_rows, spec.group, x, xs)
+            got = y.cpu().numpy().astype(np.float64)[:, rows]
+            err = np.abs(got - ref)
+            allowed = 1e-3 * kbar if kind == "bf16" else 1e-5 * gbar
+            ratio = float(np.max(err / (allowed + 1e-30)))
+            worst = max(worst, ratio)
+            rows_checked += got.size
+            if not np.all(err <= allowed + 1e-30) or not np.all(np.isfinite(got)):
+                ok = False
+    return ok, rows_checked, worst
+
+
+# ---------------------------------------------------------------------------
+# One layer set
+# ---------------------------------------------------------------------------
+
+def describe_workload(wk, layers, m):
+    mats = wk.matrices
+    z = (f"per-row z ~ U[{mats[0].row_z[0]}, {mats[0].row_z[1]}]" if mats[0].row_z else f"z={mats[0].z} iid")
+    return (f"{wk.name}: {layers} layers x {{q,o {mats[0].n}x{mats[0].k}; k,v {mats[1].n}x{mats[1].k}; "
+            f"gate,up {mats[4].n}x{mats[4].k}; down {mats[6].n}x{mats[6].k}}}, {z}, "
+            f"{'per-tensor' if mats[0].group == 0 else 'group-128'} fp16 scales, batch {m}")
+
+
+def run_workload(name, args, m, fmts, check=True, say=None):
+    """Time the step of one layer set in every format and activation type.
+
+    Returns a dict with the per-format step times, bytes, the self-check
+    result, and what the dominant-launch roofline needs."""
+    from paper_2609_16338_amd import _native as N
+
+    say = say or (lambda *a: print("[bench]", *a, file=sys.stderr, flush=True))
+    wk = wl.WORKLOADS[name]
+    layers = args.layers or wk.layers
+    t0 = time.perf_counter()
+    samples = {} if check else None
+    packed = build_set(wk, layers, fmts, args.threads, samples)
+    acts, xhost = activations(wk, ("bf16", "int8"), m)
+    say(f"{name}: packed {layers} layers x {len(wk.matrices)} matrices in {time.perf_counter() - t0:.1f} s")
+
+    payload = {fmt: sum(e[3].payload_bits for e in ents) / 8 for fmt, ents in packed.items()}
+    total = {fmt: sum(e[3].total_bytes for e in ents) for fmt, ents in packed.items()}
+    res, checks, unsupported = {}, {}, {}
+    copies = max(1, args.copies)
+    keep_sets = None
+    for fmt in fmts:
+        sets = device_copies(packed[fmt], copies)
+        for kind in ("bf16", "int8"):
+            if not supported(packed[fmt], kind, m):
+                if fmt == N.FMT_BITCOS:
+                    raise SystemExit(f"no BITCOS kernel for {name} with {kind} activations at batch {m}")
+                res[(fmt, kind)] = None
+                unsupported[f"{FMT_NAMES[fmt]}_{kind}"] = "no kernel for rows this long (K > 16384 with bf16 activations)"
+                say(f"{name} {FMT_NAMES[fmt]} {kind}: no kernel for this set, skipped")
+                continue
+            steps = [make_step(st, acts, kind) for st in sets]
+            gs = [capture(s) for s, _ in steps]
+            ms = time_graphs(gs, args.steps, args.warmup, args.warm_ms)
+            res[(fmt, kind)] = ms
+            if check:
+                rows_checked, worst, good = 0, 0.0, True
+                for _, batches in steps:
+                    g_ok, nrows, w_ = check_outputs(batches, samples, xhost, kind)
+                    good &= g_ok
+                    rows_checked += nrows
+                    worst = max(worst, w_)
+                checks[f"{FMT_NAMES[fmt]}_{kind}"] = {"ok": good, "outputs_checked": rows_checked,
+                                                      "worst_error_over_allowed": round(worst, 6)}
+                if not good:
+                    say(f"{name} {FMT_NAMES[fmt]} {kind}: OUTPUTS DIFFER from the dense definition "
+                        f"(worst error / allowed = {worst:.3g})")
+            say(f"{name} {FMT_NAMES[fmt]} {kind}: {ms * 1e3:.1f} us/step, {payload[fmt] / (ms * 1e-3) / 1e9:.1f} GB/s"
+                + (f", self-check {'ok' if checks[f'{FMT_NAMES[fmt]}_{kind}']['ok'] else 'FAILED'}" if check else ""))
+            del gs, steps
+        if fmt == N.FMT_BITCOS:
+            keep_sets = sets
+        del sets
+    return {"wk": wk, "layers": layers, "m": m, "packed": packed, "acts": acts, "payload": payload,
+            "total": total, "res": res, "checks": checks, "unsupported": unsupported, "bitcos_sets": keep_sets}
+
+
+def summary(r, fmts):
+    """The reported numbers of one layer set (value = BITCOS bf16)."""
+    from paper_2609_16338_amd import _native as N
+
+    res, payload, total, m = r["res"], r["payload"], r["total"], r["m"]
+    packed = r["packed"]
+    weights = sum(e[3].n * e[3].k for e in packed[N.FMT_BITCOS])
+    ms = res[(N.FMT_BITCOS, "bf16")]
+    ms8 = res[(N.FMT_BITCOS, "int8")]
+    value = payload[N.FMT_BITCOS] / (ms * 1e-3) / 1e9
+
+    def ratio(fmt, kind, t):
+        v = res.get((fmt, kind))
+        return None if v is None else round(v / t, 4)
+
+    out = {
+        "value": round(value, 2),
+        "ms_per_step": round(ms, 5),
+        "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
+        "weights_per_s": float(f"{weights / (ms * 1e-3):.4g}"),
+        "bpw_payload": round(payload[N.FMT_BITCOS] * 8 / weights, 5),
+        "bpw_total": round(total[N.FMT_BITCOS] * 8 / weights, 5),
+        "total_bytes_GBs": round(total[N.FMT_BITCOS] / (ms * 1e-3) / 1e9, 2),
+    }
+    if N.FMT_TRIT5 in fmts:
+        out["speedup_vs_trit5"] = ratio(N.FMT_TRIT5, "bf16", ms)
+        out["speedup_vs_bit2"] = ratio(N.FMT_BIT2, "bf16", ms)
+        out["baselines_us_per_step"] = {
+            f"{FMT_NAMES[f]}_{kind}": None if res[(f, kind)] is None else round(res[(f, kind)] * 1e3, 2)
+            for f in (N.FMT_TRIT5, N.FMT_BIT2) for kind in ("bf16", "int8")}
+        # Time ratios above; the byte ratios they compare against, on the
+        # formats' payload (symbols + scales) and on whole blobs (payload +
+        # sign offsets, padding and alignment).
+        out["byte_ratio_payload"] = {f"{FMT_NAMES[f]}_over_bitcos": round(payload[f] / payload[N.FMT_BITCOS], 4)
+                                     for f in (N.FMT_TRIT5, N.FMT_BIT2)}
+        out["byte_ratio_total"] = {f"{FMT_NAMES[f]}_over_bitcos": round(total[f] / total[N.FMT_BITCOS], 4)
+                                   for f in (N.FMT_TRIT5, N.FMT_BIT2)}
+        if m > 1:
+            out["baselines_note"] = f"no small-batch kernel: {m} batch-1 launches per tile and step"
+        if r["unsupported"]:
+            out["baselines_unsupported"] = r["unsupported"]
+    out["int8_variant"] = {
+        "value": round(payload[N.FMT_BITCOS] / (ms8 * 1e-3) / 1e9, 2),
+        "ms_per_step": round(ms8, 5),
+        "speedup_vs_trit5": ratio(N.FMT_TRIT5, "int8", ms8),
+        "speedup_vs_bit2": ratio(N.FMT_BIT2, "int8", ms8),
+    }
+    if r["checks"]:
+        out["self_check"] = r["checks"]
+    return out
+
+
+def dominant_roofline(r, args, name):
+    """The persistent launch carrying most of the step's bytes (bf16), timed
+    alone: ten back-to-back launches per graph replay, over the device copies
+    in turn (inside a graph consecutive kernels start without a gap)."""
+    from paper_2609_16338_amd import _native as N
+    from paper_2609_16338_amd import api
+
+    m = r["m"]
+    tops = [make_batches(st, r["acts"], "bf16")[0] for st in r["bitcos_sets"]]
+    top = tops[0]
+    reps = 10
+    gg = capture(lambda: [tops[i % len(tops)].run() for i in range(reps)])
+    ms_g = time_graph(gg, args.steps, args.warmup, args.warm_ms)
+    per_launch_us = ms_g * 1e3 / reps
+    sclk = gpu_clock_under_load(gg)
+    alg_bytes = sum(e[3].payload_bits / 8 + m * (e[3].k * 2 + e[3].n * 4) for e in top.entries)
+    achieved = alg_bytes / (per_launch_us * 1e-6) / 1e9
+    # Two-term roofline in CU-cycles per 32 weights (nominal clock): the
+    # launch's measured time against the time its bytes take at peak HBM
+    # bandwidth.  The operation sits under the HBM roofline (about 3
+    # operations per byte); the larger term says what limits this kernel.
+    top_weights = sum(e[3].n * e[3].k for e in top.entries)
+    launch_gamma = 32 * CU_COUNT * CLOCK_HZ * per_launch_us * 1e-6 / top_weights
+    hbm_term = 32 * alg_bytes / top_weights / (HBM_PEAK_GBS * 1e9 / (CU_COUNT * CLOCK_HZ))
+    kinds = {api.describe(e[3], m, N.X_BF16).kernel for e in top.entries}
+    kname = {N.KERNEL_MATRIX: "bitcos_diag_kernel", N.KERNEL_STREAMING: "bitcos_fast_kernel",
+             N.KERNEL_GENERAL: "bitcos_gemv_kernel", N.KERNEL_SMALL_BATCH: "bitcos_mfma_kernel",
+             }.get(kinds.pop(), "?") if len(kinds) == 1 else "mixed"
+    return {
+        "bound": "hbm",
+        "achieved": round(achieved, 2),
+        "peak": HBM_PEAK_GBS,
+        "unit": "GB/s",
+        "frac": round(achieved / HBM_PEAK_GBS, 4),
+        "traffic": stored_traffic(name),
+        "kernel": f"{kname}<{top.tile[0]},{top.tile[1]},bf16,table>: {len(top.entries)} GEMVs in one launch",
+        "per_launch_us": round(per_launch_us, 3),
+        "bytes_per_launch": int(alg_bytes),
+        "weights_per_launch": int(top_weights),
+        "two_term": {"cu_cycles_per_32w": round(launch_gamma, 4), "hbm_cu_cycles_per_32w": round(hbm_term, 4),
+                     "larger_term": "instructions" if launch_gamma > hbm_term else "hbm"},
+    }, sclk
 
 
 def cpu_model():
@@ -382,6 +659,10 @@ def cpu_baseline(wk, budget_s=12.0):
     }
 
 
+# ---------------------------------------------------------------------------
+# Other modes
+# ---------------------------------------------------------------------------
+
 def profile_pass(args):
     """Counter runs: the dominant launch of the headline step, then a plain copy
     of known size whose FETCH_SIZE / WRITE_SIZE calibrate the counters."""
@@ -392,7 +673,7 @@ def profile_pass(args):
     wk = wl.WORKLOADS[args.workload]
     layers = args.layers or wk.layers
     packed = build_set(wk, layers, [N.FMT_BITCOS], args.threads)
-    acts = activations(wk, ("bf16",))
+    acts, _ = activations(wk, ("bf16",))
     top = make_batches(packed[N.FMT_BITCOS], acts, "bf16")[0]
     for _ in range(5):
         top.run()
@@ -404,9 +685,26 @@ def profile_pass(args):
         dst.copy_(src)
     torch.cuda.synchronize()
     alg = sum(e[3].payload_bits / 8 + e[3].k * 2 + e[3].n * 4 for e in top.entries)
-    print(f"[profile-pass] dominant launch: {len(top.entries)} GEMVs, tile {top.tile}, "
+    print(f"[profile-pass] {args.workload} dominant launch: {len(top.entries)} GEMVs, tile {top.tile}, "
           f"algorithmic bytes {int(alg)}; copy {COPY_MIB} MiB; kernel_source_hash {kernel_source_hash()}",
           flush=True)
+
+
+def hbm_read(args):
+    """Plain streaming-read bandwidth: a max-reduction over a 4 GiB int32
+    tensor (torch's reduction kernel reads every byte once and writes one
+    value), timed from a graph of ten back-to-back reductions."""
+    import torch
+    nbytes = 4 << 30
+    x = torch.randint(-1000, 1000, (nbytes // 4,), dtype=torch.int32, device="cuda")
+    out = torch.empty((), dtype=torch.int32, device="cuda")
+    reps = 10
+    g = capture(lambda: [torch.amax(x, dim=0, out=out) for _ in range(reps)])
+    ms = time_graph(g, 20, 5, args.warm_ms)
+    gbs = reps * nbytes / (ms * 1e-3) / 1e9
+    emit({"metric": "plain streaming read bandwidth (torch amax over 4 GiB int32)", "value": round(gbs, 1),
+          "unit": "GB/s", "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4), "bytes_per_read": nbytes,
+          "ms_per_read": round(ms / reps, 4)}, args)
 
 
 def sweep(args):
@@ -434,12 +732,13 @@ def sweep(args):
             src = torch.from_numpy(blob).cuda()
             blobs = [src.clone() for _ in range(args.sweep_copies)]
             row[f"{nm}_payload_bytes"] = L.payload_bits // 8
+            row[f"{nm}_total_bytes"] = L.total_bytes
             row[f"{nm}_bpw"] = round(L.payload_bits / (spec.n * spec.k), 5)
             for kind, x in (("int8", xi), ("bf16", xb)):
                 ys = [torch.empty(spec.n, dtype=torch.float32, device="cuda") for _ in blobs]
                 b = api.Batch([L] * len(blobs), blobs, [x] * len(blobs), ys)
                 g = capture(b.run)
-                ms, _ = time_graph(g, args.steps, args.warmup)
+                ms = time_graph(g, args.steps, args.warmup, args.warm_ms)
                 us = ms * 1e3 / len(blobs)
                 row[f"{nm}_{kind}_us"] = round(us, 4)
                 row[f"{nm}_{kind}_GBs"] = round(L.payload_bits / 8 / (us * 1e-6) / 1e9, 1)
@@ -464,7 +763,7 @@ def sweep(args):
                 return round(z0 + (1 - s0) * (z1 - z0) / (s1 - s0), 4)
         return None
 
-    print(json.dumps({
+    emit({
         "metric": "zero-density sweep, 8192x8192 g128, batch 1: per-GEMV time, effective GB/s, speedups",
         "unit": "us",
         "copies_per_launch": args.sweep_copies,
@@ -474,12 +773,10 @@ def sweep(args):
         "crossover_z_vs_trit5_int8": crossover("int8"),
         "crossover_z_vs_trit5_bf16": crossover("bf16"),
         "points": rows,
-    }))
+    }, args)
 
 
 GAMMA_Z = (0.30, 0.42, 0.515, 0.95)
-CU_COUNT = 256
-CLOCK_HZ = 2.4e9
 
 
 def gamma(args):
@@ -489,9 +786,9 @@ def gamma(args):
     L2-resident (one launch over 64 GEMVs that all read the same 2048 x 8192
     g128 blob, 3.6-4.4 MB, which each XCD's 4 MB L2 holds, so the instruction
     stream is the limit and the kernel's prologue is amortised); beta = HBM
-    bytes per CU-cycle at the
-    8 TB/s peak; B(z) = bytes per 32 weights of each layout.  Predicted
-    effective bandwidth = min(beta, B / gamma) per CU, times all CUs."""
+    bytes per CU-cycle at the 8 TB/s peak; B(z) = bytes per 32 weights of each
+    layout.  Predicted effective bandwidth = min(beta, B / gamma) per CU,
+    times all CUs."""
     import torch
 
     from paper_2609_16338_amd import _native as N
@@ -518,7 +815,7 @@ def gamma(args):
                 ys = [torch.empty(n, dtype=torch.float32, device="cuda") for _ in range(reps)]
                 b = api.Batch([L] * reps, devs, [x] * reps, ys)
                 g = capture(b.run)
-                ms, _ = time_graph(g, max(args.steps, 50), args.warmup)
+                ms = time_graph(g, max(args.steps, 50), args.warmup, args.warm_ms)
                 rate = reps * n * k / (ms * 1e-3)
                 gam = 32 * CU_COUNT * CLOCK_HZ / rate
                 row[f"{nm}_{kind}_gamma"] = round(gam, 3)
@@ -529,18 +826,25 @@ def gamma(args):
         rows.append(row)
         print(f"[gamma] z={z}: " + ", ".join(f"{nm} {row[f'{nm}_int8_gamma']:.2f}/{row[f'{nm}_bf16_gamma']:.2f}"
                                             for nm in names.values()), file=sys.stderr, flush=True)
-    print(json.dumps({
+    emit({
         "metric": "two-term roofline: gamma = CU-cycles per 32 weights, L2-resident 2048x8192 g128 (x64 per launch), batch 1",
         "beta_bytes_per_cu_cycle": round(beta, 4),
         "clock_hz": CLOCK_HZ,
         "cus": CU_COUNT,
         "data": "synthetic",
         "points": rows,
-    }))
+    }, args)
 
 
-def main():
-    args = parse()
+# ---------------------------------------------------------------------------
+# Headline
+# ---------------------------------------------------------------------------
+
+def main(argv=None):
+    args = parse(argv)
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        sys.exit(2)
     if args.gamma:
         gamma(args)
         return
@@ -550,158 +854,77 @@ def main():
     if args.sweep:
         sweep(args)
         return
-    if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
-        sys.exit(2)
+    if args.hbm_read:
+        hbm_read(args)
+        return
     import torch
 
     from paper_2609_16338_amd import _native as N
-    from paper_2609_16338_amd import api
 
     N.lib()
     assert torch.cuda.is_available(), "bench.py needs a GPU"
-    wk = wl.WORKLOADS[args.workload]
-    layers = args.layers or wk.layers
     m = args.batch
     if not 1 <= m <= 16:
         print(json.dumps({"error": "--batch must be in 1..16"}))
         sys.exit(2)
     fmts = [N.FMT_BITCOS] + ([] if args.no_baselines else [N.FMT_TRIT5, N.FMT_BIT2])
-    t0 = time.perf_counter()
-    packed = build_set(wk, layers, fmts, args.threads)
-    acts = activations(wk, ("bf16", "int8"), m)
-    prep_s = time.perf_counter() - t0
-    print(f"[bench] packed {layers} layers x {len(wk.matrices)} matrices in {prep_s:.1f} s", file=sys.stderr, flush=True)
+    check = not args.no_check
 
-    payload = {fmt: sum(e[3].payload_bits for e in ents) / 8 for fmt, ents in packed.items()}
+    r = run_workload(args.workload, args, m, fmts, check)
+    head = summary(r, fmts)
+    roof, sclk = dominant_roofline(r, args, args.workload)
+    wk, layers = r["wk"], r["layers"]
+    packed = r["packed"]
     weights = sum(e[3].n * e[3].k for e in packed[N.FMT_BITCOS])
-    res = {}
-    unsupported = {}
-    copies = max(1, args.copies)
-    bitcos_sets = None
-    warmed = False
-    for fmt in fmts:
-        sets = device_copies(packed[fmt], copies)
-        for kind in ("bf16", "int8"):
-            if not supported(packed[fmt], kind, m):
-                if fmt == N.FMT_BITCOS:
-                    raise SystemExit(f"no BITCOS kernel for this set with {kind} activations at batch {m}")
-                res[(fmt, kind)] = None
-                unsupported[f"{FMT_NAMES[fmt]}_{kind}"] = "no kernel for rows this long (K > 16384 with bf16 activations)"
-                print(f"[bench] fmt={fmt} {kind}: no kernel for this set, skipped", file=sys.stderr, flush=True)
-                continue
-            gs = [capture(make_step(st, acts, kind)[0]) for st in sets]
-            if not warmed:
-                warmed = True
-                n, wms = warm_device(gs[0])
-                print(f"[bench] device warm-up: {n} untimed replays in {wms:.0f} ms", file=sys.stderr, flush=True)
-            ms, wall = time_graphs(gs, args.steps, args.warmup)
-            res[(fmt, kind)] = ms
-            print(f"[bench] fmt={fmt} {kind}: {ms * 1e3:.1f} us/step, "
-                  f"{payload[fmt] / (ms * 1e-3) / 1e9:.1f} GB/s", file=sys.stderr, flush=True)
-            del gs
-        if fmt == N.FMT_BITCOS:
-            bitcos_sets = sets
-        del sets
-
-    # Dominant kernel: the batched BITCOS launch carrying most of the bytes
-    # (the K = 2560 tile for this set: q, k, v, o, gate, up of every layer),
-    # timed alone.
-    tops = [make_batches(st, acts, "bf16")[0] for st in bitcos_sets]
-    top = tops[0]
-    # Ten back-to-back launches per replay, over the device copies in turn:
-    # inside a graph consecutive kernels start without a gap, so replay
-    # overhead stays out of the per-launch time.
-    reps = 10
-    gg = capture(lambda: [tops[i % len(tops)].run() for i in range(reps)])
-    ms_g, _ = time_graph(gg, args.steps, args.warmup)
-    per_launch_us = ms_g * 1e3 / reps
-    sclk = gpu_clock_under_load(gg)
-    alg_bytes = sum(e[3].payload_bits / 8 + m * (e[3].k * 2 + e[3].n * 4) for e in top.entries)
-    achieved = alg_bytes / (per_launch_us * 1e-6) / 1e9
-    # Two-term roofline of the launch in CU-cycles per 32 weights (nominal
-    # clock): its measured time against the time its bytes take at peak HBM
-    # bandwidth; the larger term binds.
-    top_weights = sum(e[3].n * e[3].k for e in top.entries)
-    launch_gamma = 32 * CU_COUNT * CLOCK_HZ * per_launch_us * 1e-6 / top_weights
-    hbm_term = 32 * alg_bytes / top_weights / (HBM_PEAK_GBS * 1e9 / (CU_COUNT * CLOCK_HZ))
-    ms = res[(N.FMT_BITCOS, "bf16")]
-    value = payload[N.FMT_BITCOS] / (ms * 1e-3) / 1e9
     out = {
         "metric": METRIC,
-        "value": round(value, 2),
+        "value": head.pop("value"),
         "unit": "GB/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms, 5),
+        "ms_per_step": head.pop("ms_per_step"),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
         "config": {
-            "workload": f"{wk.name}: {layers} layers x {{q,o {wk.matrices[0].n}x{wk.matrices[0].k}; "
-                        f"k,v {wk.matrices[1].n}x{wk.matrices[1].k}; gate,up {wk.matrices[4].n}x{wk.matrices[4].k}; "
-                        f"down {wk.matrices[6].n}x{wk.matrices[6].k}}}, z={wk.matrices[0].z} iid, "
-                        f"{'per-tensor' if wk.matrices[0].group == 0 else 'group-128'} fp16 scales, "
-                        f"bf16 x ~ N(0,1), batch {m}",
+            "workload": describe_workload(wk, layers, m) + ", bf16 x ~ N(0,1)",
             "global_batch": m,
             "layers": layers,
             "gemvs_per_step": len(packed[N.FMT_BITCOS]),
             "weights_per_step": weights,
-            "payload_bytes_per_step": int(payload[N.FMT_BITCOS]),
-            "total_bytes_per_step": int(sum(e[3].total_bytes + m * (e[3].k * 2 + e[3].n * 4)
-                                            for e in packed[N.FMT_BITCOS])),
-            "device_copies": copies,
+            "payload_bytes_per_step": int(r["payload"][N.FMT_BITCOS]),
+            "total_bytes_per_step": int(r["total"][N.FMT_BITCOS]
+                                        + sum(m * (e[3].k * 2 + e[3].n * 4) for e in packed[N.FMT_BITCOS])),
+            "device_copies": max(1, args.copies),
+            "warm_ms_per_format": args.warm_ms,
         },
-        "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
-        "weights_per_s": float(f"{weights / (ms * 1e-3):.4g}"),
-        "bpw_payload": round(payload[N.FMT_BITCOS] * 8 / weights, 5),
     }
-    def ratio(fmt, kind, t):
-        v = res.get((fmt, kind))
-        return None if v is None else round(v / t, 4)
-
-    ms8 = res[(N.FMT_BITCOS, "int8")]
-    if N.FMT_TRIT5 in fmts:
-        out["speedup_vs_trit5"] = ratio(N.FMT_TRIT5, "bf16", ms)
-        out["speedup_vs_bit2"] = ratio(N.FMT_BIT2, "bf16", ms)
-        out["baselines_us_per_step"] = {
-            f"{FMT_NAMES[f]}_{kind}": None if res[(f, kind)] is None else round(res[(f, kind)] * 1e3, 2)
-            for f in (N.FMT_TRIT5, N.FMT_BIT2) for kind in ("bf16", "int8")}
-        if m > 1:
-            out["baselines_note"] = f"no small-batch kernel: {m} batch-1 launches per tile and step"
-        if unsupported:
-            out["baselines_unsupported"] = unsupported
-    out["int8_variant"] = {
-        "value": round(payload[N.FMT_BITCOS] / (ms8 * 1e-3) / 1e9, 2),
-        "ms_per_step": round(ms8, 5),
-        "speedup_vs_trit5": ratio(N.FMT_TRIT5, "int8", ms8),
-        "speedup_vs_bit2": ratio(N.FMT_BIT2, "int8", ms8),
-    }
-    # The kernel the launcher picks (all GEMVs of the launch share layout kind and tile).
-    kinds = {api.describe(e[3], m, N.X_BF16).kernel for e in top.entries}
-    kname = {N.KERNEL_MATRIX: "bitcos_diag_kernel", N.KERNEL_STREAMING: "bitcos_fast_kernel",
-             N.KERNEL_GENERAL: "bitcos_gemv_kernel", N.KERNEL_SMALL_BATCH: "bitcos_mfma_kernel",
-             }.get(kinds.pop(), "?") if len(kinds) == 1 else "mixed"
-    out["roofline"] = {
-        "bound": "hbm",
-        "achieved": round(achieved, 2),
-        "peak": HBM_PEAK_GBS,
-        "unit": "GB/s",
-        "frac": round(achieved / HBM_PEAK_GBS, 4),
-        "traffic": stored_traffic(),
-        "kernel": f"{kname}<{top.tile[0]},{top.tile[1]},bf16,table>: {len(top.entries)} GEMVs in one launch",
-        "per_launch_us": round(per_launch_us, 3),
-        "bytes_per_launch": int(alg_bytes),
-        "two_term": {"cu_cycles_per_32w": round(launch_gamma, 4), "hbm_cu_cycles_per_32w": round(hbm_term, 4),
-                     "binds": "instructions" if launch_gamma > hbm_term else "hbm"},
-    }
+    out.update(head)
+    out["roofline"] = roof
     out["sclk_mhz_under_load"] = sclk
+    failed = [k for k, v in r["checks"].items() if not v["ok"]]
+    del r
+    torch.cuda.empty_cache()
+
+    extras = {}
+    for name in [s for s in args.extra.split(",") if s and s != args.workload]:
+        re_ = run_workload(name, args, m, fmts, check)
+        extras[name] = dict(workload=describe_workload(re_["wk"], re_["layers"], m), **summary(re_, fmts))
+        failed += [f"{name}:{k}" for k, v in re_["checks"].items() if not v["ok"]]
+        del re_
+        torch.cuda.empty_cache()
+    if extras:
+        out["extra_workloads"] = extras
+    if failed:
+        print(json.dumps({"error": "self-check failed: GPU outputs differ from the dense definition",
+                          "failed": failed}), flush=True)
+        sys.exit(3)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wk)
-    print(json.dumps(out))
+    emit(out, args)
 
 
 if __name__ == "__main__":

@@ -99,3 +99,47 @@ def test_main_shadows_no_module_function():
     funcs = {n for n, v in vars(bench).items() if inspect.isfunction(v)}
     for fn in (bench.main,):
         assert not (set(fn.__code__.co_varnames) & funcs), set(fn.__code__.co_varnames) & funcs
+
+
+def test_sample_rows_keep_first_and_last():
+    for n in (1, 2, 5, 640, 25600):
+        rows = bench.sample_rows(n, 3, 4)
+        assert rows[0] == 0 and rows[-1] == n - 1
+        assert len(set(rows.tolist())) == len(rows) <= max(bench.SAMPLE_ROWS, 1)
+        assert np_all_in_range(rows, n)
+
+
+def np_all_in_range(rows, n):
+    return bool(((rows >= 0) & (rows < n)).all())
+
+
+@pytest.mark.parametrize("group", [128, 0])
+@pytest.mark.parametrize("kind", ["bf16", "int8"])
+def test_self_check_reference_matches_the_oracle(group, kind):
+    """bench.py's self-check reference (dense definition on sampled rows)
+    agrees with the oracle's dense GEMV, and its error bars with the parity
+    tests' bars."""
+    np = pytest.importorskip("numpy")
+    import oracle as O
+    import workloads as wl
+    from parity_checks import bf16_bound, group_bound
+
+    n, k, m = 37, 640, 3
+    w = wl.ternary(n, k, 0.45, wl.rng_for(70, group))
+    ns = n * (k // 128) if group == 128 else 1
+    sc = wl.fp16_uniform((ns,), 0.005, 0.05, wl.rng_for(71, group))
+    rows = bench.sample_rows(n, 1, 2)
+    sbits = sc.reshape(n, k // 128)[rows] if group == 128 else sc.reshape(1, 1)
+    if kind == "bf16":
+        xb = wl.act_bf16(m, k, wl.rng_for(72))
+        ref = O.dense_gemv(w, sc, group, xb, x_is_bf16_bits=True)[:, rows]
+        y, kbar, _ = bench.dense_rows(w[rows], sbits, group, bench.bf16_bits_to_f64(xb).reshape(m, k), None)
+        bound = bf16_bound(w[rows], sc if group == 0 else sbits.reshape(-1), group, xb)
+        assert np.allclose(kbar, bound, rtol=1e-12)
+    else:
+        q, a = O.quantize_activations(wl.act_bf16(m, k, wl.rng_for(73)))
+        ref = O.dense_gemv(w, sc, group, q, a)[:, rows]
+        y, _, gbar = bench.dense_rows(w[rows], sbits, group, q.astype(np.float64), a.astype(np.float64))
+        bound = group_bound(w[rows], sc if group == 0 else sbits.reshape(-1), group, q, a)
+        assert np.allclose(gbar, bound, rtol=1e-12)
+    assert np.array_equal(y.astype(np.float32), ref)

@@ -396,6 +396,12 @@ def test_roofline_bytes_and_table2():
         assert 6.9 / float(r["gamma"]) == pytest.approx(float(r["b_over_gamma"]), rel=5e-3)
         assert bound == r["bound"]
         assert e == pytest.approx(min(float(r["beta"]), float(r["b_over_gamma"])), rel=5e-3)
+        # Eq. (6): the effective bandwidth is the iteration's bytes over its
+        # time, and neither term of Eq. (5) can be beaten: T >= gamma and
+        # T >= B / beta, with equality in the term the row is bound by.
+        assert t * e == pytest.approx(6.9, rel=1e-12)
+        assert t >= float(r["gamma"]) - 1e-12 and t >= 6.9 / float(r["beta"]) - 1e-12
+        assert t == pytest.approx(float(r["gamma"]) if bound == "instructions" else 6.9 / float(r["beta"]))
 
 
 # ---------------------------------------------------------------------------
