@@ -1,4 +1,4 @@
-"""GPU: the device-side BITCOS packer against the host packer.
+"""GPU: the device-side BITCOS packer against the host packer and the oracle.
 
 The host packer writes exactly the oracle's bytes (test_host_lib.py); the
 device packer must produce the same layout and the same blob bytes for every
@@ -67,6 +67,9 @@ def test_device_pack_matches_host(n, k, z, group, unit):
     assert got.shape == blob_h.shape
     bad = np.flatnonzero(got != blob_h)
     assert bad.size == 0, f"{bad.size} bytes differ, first at {bad[:8]}"
+    # and the oracle's own serialised blob, byte for byte
+    ob, _ = O.serialize(O.bitcos_encode(w, sc, group, Lh.unit_rows))
+    assert np.array_equal(got, np.frombuffer(ob, dtype=np.uint8))
 
 
 def test_device_pack_full_size_and_gemv():

@@ -52,6 +52,16 @@ def launch_units(b):
     return int(b.host[32:40].view(np.int64)[0])
 
 
+HEADER_FIELDS = {"unit_is_step": 40, "m": 44, "any_xscale": 48, "any_grouped": 52, "row_offsets": 56,
+                 "small_batch": 60}
+
+
+def header_flag(b, name):
+    """An int32 field of a batch's host table header (batch.h, BatchHeader)."""
+    o = HEADER_FIELDS[name]
+    return int(b.host[o:o + 4].view(np.int32)[0])
+
+
 def oracle_acts(wk, m=1):
     """Device activations: bf16 from the seeded generator, int8 + per-group
     scales from the oracle's quantiser; host copies for the references."""
@@ -132,8 +142,12 @@ def test_bitnet_step_as_timed(bitnet_set, fmt, kind):
     batches = bench.make_batches(packed[fmt], acts, kind)
     say("bitnet", FMT_NAME(packed[fmt][0][3]), kind, [(b.tile, b.count, launch_units(b)) for b in batches])
     if fmt == N.FMT_BITCOS:
-        want = N.KERNEL_MATRIX if kind == "bf16" else N.KERNEL_STREAMING
-        assert all(b.kernel == want for b in batches)
+        # describe() names the kernel of a call without activation scales: the
+        # matrix-core kernel for these per-tensor layouts.  The int8 variant
+        # carries activation scales (header flag), which the launcher sends
+        # to the streaming kernel instead.
+        assert all(b.kernel == N.KERNEL_MATRIX for b in batches)
+        assert all(header_flag(b, "any_xscale") == (kind == "int8") for b in batches)
     assert check_batches(batches, samples, host, kind) == len(packed[fmt])
 
 
