@@ -48,7 +48,8 @@
  *     device work is enqueued.
  *   - The caller owns every host and device buffer and the stream; the
  *     library allocates nothing on the device, keeps no mutable global state
- *     and is safe to call from several threads.
+ *     and is safe to call from several threads.  The one exception is the
+ *     fixed per-GPU workspace of bitcos_pack_device_noalloc (see there).
  *   - Device pointers are plain device addresses (e.g. a torch tensor's
  *     data_ptr()); `stream` is a hipStream_t passed as void* (NULL = the
  *     default stream).  GEMV calls are asynchronous and never synchronise.
@@ -260,6 +261,30 @@ int bitcos_plan_device(const int8_t* w_dev, int32_t n, int32_t k, int32_t group,
                        void* ws_dev, size_t ws_bytes, bitcos_layout* out, void* stream);
 int bitcos_pack_device(const int8_t* w_dev, const uint16_t* scales_dev, const bitcos_layout* L,
                        void* ws_dev, size_t ws_bytes, void* dst_dev, size_t cap, void* stream);
+
+/* ---- device-side packing without allocation ------------------------------
+ * For callers that cannot allocate device memory (code under graph capture
+ * of its neighbours, serving loops and harnesses that forbid hipMalloc):
+ * bitcos_plan_device + bitcos_pack_device in one call, with the plan's
+ * workspace in a fixed array the library keeps in every GPU it runs on
+ * (about 1 MiB each, held until the process ends) instead of a caller
+ * buffer.  Nothing is allocated: the caller passes W, the scales and dst.
+ *
+ * bitcos_pack_device_noalloc: W device int8 [n][k], scales_dev device fp16
+ *   ([n][k/128] or [1]), group / unit_rows as bitcos_plan; fills *out as
+ *   bitcos_plan would and writes the blob into dst_dev (cap bytes) -- the
+ *   same bytes as bitcos_pack.  Waits for `stream` before returning (the
+ *   plan reads the non-zero count back).
+ *   Errors: E_ARG, E_SPACE (n > BITCOS_NOALLOC_MAX_ROWS, checked before any
+ *   device work; or cap < out->total_bytes, with *out filled so the caller
+ *   can size dst and call again), E_VALUE, E_UNSUPPORTED, E_HIP.
+ *   Every call on one GPU uses that GPU's one workspace: calls that overlap
+ *   in time on one GPU (other threads, other streams) race and must be
+ *   serialised by the caller; calls on different GPUs do not interact. */
+#define BITCOS_NOALLOC_MAX_ROWS 262144
+int bitcos_pack_device_noalloc(const int8_t* w_dev, const uint16_t* scales_dev, int32_t n, int32_t k,
+                               int32_t group, int32_t unit_rows, bitcos_layout* out, void* dst_dev, size_t cap,
+                               void* stream);
 
 /* ---- launch description (for measurement) ---------------------------------
  * Fills the kernel configuration a GEMV on this layout would launch with,

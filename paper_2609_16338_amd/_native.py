@@ -25,6 +25,7 @@ SEC_CODES = 0
 X_I8, X_BF16 = 1, 2
 Y_F32, Y_I32_RAW = 1, 2
 MAX_M = 16  # most activation rows per GEMV call
+NOALLOC_MAX_ROWS = 262144  # rows bitcos_pack_device_noalloc's fixed workspace holds
 KERNEL_GENERAL, KERNEL_STREAMING, KERNEL_MATRIX, KERNEL_SMALL_BATCH, KERNEL_FIXED = 1, 2, 3, 4, 5
 LAYOUT_VERSION = 1
 
@@ -100,6 +101,7 @@ SIGNATURES = {
     "bitcos_plan_device_workspace": (ctypes.c_size_t, [_I32]),
     "bitcos_plan_device": (ctypes.c_int, [_P, _I32, _I32, _I32, _I32, _P, _SZ, _LP, _P]),
     "bitcos_pack_device": (ctypes.c_int, [_P, _P, _LP, _P, _SZ, _P, _SZ, _P]),
+    "bitcos_pack_device_noalloc": (ctypes.c_int, [_P, _P, _I32, _I32, _I32, _I32, _LP, _P, _SZ, _P]),
 }
 
 

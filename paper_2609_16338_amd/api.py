@@ -146,6 +146,35 @@ def bitcos_pack_device(w_dev, scales_dev, group: int = 128, unit_rows: int = 0, 
     return L, blob
 
 
+def bitcos_pack_device_noalloc(w_dev, scales_dev, dst_dev, group: int = 128, unit_rows: int = 0, stream=None):
+    """Layout of W packed on the GPU into the caller's dst_dev (a uint8 cuda
+    tensor), with the library's fixed per-GPU workspace: no device memory is
+    allocated by the call.  Raises BitcosError(E_SPACE) if dst_dev is too
+    small (its .status tells; the layout needed is in the exception's
+    `layout`)."""
+    import torch
+    if w_dev.dtype != torch.int8 or w_dev.dim() != 2 or not w_dev.is_cuda or not w_dev.is_contiguous():
+        raise ValueError("w_dev must be a contiguous 2-D int8 CUDA tensor")
+    if scales_dev.dtype not in (torch.float16, torch.int16) or not scales_dev.is_cuda or not scales_dev.is_contiguous():
+        raise ValueError("scales_dev must be a contiguous fp16 CUDA tensor")
+    if dst_dev.dtype != torch.uint8 or not dst_dev.is_cuda or not dst_dev.is_contiguous():
+        raise ValueError("dst_dev must be a contiguous uint8 CUDA tensor")
+    n, k = w_dev.shape
+    ns = n * (k // 128) if group == 128 else 1
+    if scales_dev.numel() != ns:
+        raise ValueError(f"scales_dev has {scales_dev.numel()} values, the layout needs {ns}")
+    L = Layout()
+    st = N.lib().bitcos_pack_device_noalloc(ctypes.c_void_p(w_dev.data_ptr()), ctypes.c_void_p(scales_dev.data_ptr()),
+                                            n, k, group, unit_rows, ctypes.byref(L),
+                                            ctypes.c_void_p(dst_dev.data_ptr()), dst_dev.numel(),
+                                            _stream_handle(stream))
+    if st:
+        err = N.BitcosError(st, "bitcos_pack_device_noalloc")
+        err.layout = L
+        raise err
+    return L
+
+
 # ---------------------------------------------------------------------------
 # GEMV (device)
 # ---------------------------------------------------------------------------

@@ -19,6 +19,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "../../include/bitcos.h"
 #include "device_common.h"
 #include "launch_common.h"
@@ -197,6 +199,33 @@ int sync_status(hipStream_t st) {
   return BITCOS_OK;
 }
 
+// Workspace of bitcos_pack_device_noalloc for matrices of up to
+// BITCOS_NOALLOC_MAX_ROWS rows: the header and n + 1 row offsets of the
+// plan.  One copy per GPU the library runs on, held until the process ends.
+constexpr size_t kNoallocBytes =
+    (sizeof(WsHeader) + 4u * (static_cast<size_t>(BITCOS_NOALLOC_MAX_ROWS) + 1) + 15u) / 16u * 16u;
+__device__ __align__(256) uint8_t scratch[kNoallocBytes];
+
+constexpr int kMaxDevices = 64;
+
+// Device address of this GPU's `scratch`, looked up once per device with
+// that device current.  The host-side name of a __device__ array is not its
+// device address; only this pointer may reach kernels and copies.
+int noalloc_workspace(void** out) {
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return BITCOS_E_HIP;
+  std::lock_guard<std::mutex> g(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return BITCOS_E_HIP;
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return BITCOS_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -258,6 +287,23 @@ int bitcos_pack_device(const int8_t* w_dev, const uint16_t* scales_dev, const bi
   st = sync_status(s);
   if (st) return st;
   return flag ? BITCOS_E_VALUE : BITCOS_OK;
+}
+
+int bitcos_pack_device_noalloc(const int8_t* w_dev, const uint16_t* scales_dev, int32_t n, int32_t k,
+                               int32_t group, int32_t unit_rows, bitcos_layout* out, void* dst_dev, size_t cap,
+                               void* stream) {
+  if (!w_dev || !scales_dev || !out || !dst_dev) return BITCOS_E_ARG;
+  int st = check_shape(n, k, group, unit_rows);
+  if (st) return st;
+  if (n > BITCOS_NOALLOC_MAX_ROWS) return BITCOS_E_SPACE;  // more rows than the fixed workspace holds
+  void* ws = nullptr;
+  st = noalloc_workspace(&ws);
+  if (st) return st;
+  const size_t ws_bytes = bitcos_plan_device_workspace(n);
+  st = bitcos_plan_device(w_dev, n, k, group, unit_rows, ws, ws_bytes, out, stream);
+  if (st) return st;
+  if (cap < out->total_bytes) return BITCOS_E_SPACE;  // *out tells the caller the size
+  return bitcos_pack_device(w_dev, scales_dev, out, ws, ws_bytes, dst_dev, cap, stream);
 }
 
 }  // extern "C"
