@@ -87,10 +87,10 @@ struct StepGen {
 };
 
 // The wave's contiguous unit range of a persistent launch; returns false if empty.
-template <int R, bool TABLE>
+template <int R, bool TABLE, int WPB = kBlock / kWave>
 __device__ __forceinline__ bool wave_range(const KernelArgs& a, StepGen<R, TABLE>& gen) {
-  const int wave = __builtin_amdgcn_readfirstlane(blockIdx.x * (kBlock / kWave) + (threadIdx.x >> 6));
-  const int64_t nwaves = static_cast<int64_t>(gridDim.x) * (kBlock / kWave);
+  const int wave = __builtin_amdgcn_readfirstlane(blockIdx.x * WPB + (threadIdx.x >> 6));
+  const int64_t nwaves = static_cast<int64_t>(gridDim.x) * WPB;
   const int64_t per = (a.total_units + nwaves - 1) / nwaves;
   gen.U = per * wave;
   gen.Uend = min(gen.U + per, a.total_units);
@@ -176,9 +176,22 @@ struct Trit5TablesI8 {
 };
 // bf16 variant: five bf16 weights starting at element 0 or 1 of a 16-byte
 // entry (an even byte of a block starts on a dword, an odd one half-way in).
+// Each entry is kept in kTrit5Copies copies (copy c of value v at index
+// v * kTrit5Copies + c; lane l reads copy l % kTrit5Copies): a ds_read_b128
+// serves 16 lanes at a time, and 16 copies keep any 16 keys on distinct
+// banks, where a single copy serialises lanes whose values share banks.
+constexpr int kTrit5Copies = 16;
 struct Trit5TablesBf16 {
-  uint4 t[2][256];
+  uint4 t[2][256 * kTrit5Copies];
 };
+
+// Workgroup size of the baselines: the five-trit bf16 kernel fills most of
+// the LDS with replicated tables, so one workgroup holds a CU's waves (three
+// per SIMD with one block per lane, two with two); the others run several
+// 256-thread workgroups per CU.  Host and device both use it.
+constexpr int fixed_threads(bool bit2, bool bf16, int per_lane) {
+  return (bit2 || !bf16) ? kBlock : (per_lane == 1 ? 768 : 512);
+}
 
 __device__ __forceinline__ void trit5_digits(int v, int (&w)[5]) {
   bool ok = v < 243;
@@ -201,15 +214,17 @@ __device__ __forceinline__ void build_trit5_i8(Trit5TablesI8& tb, int v) {
   }
 }
 
-__device__ __forceinline__ void build_trit5_bf16(Trit5TablesBf16& tb, int v) {
-  int w[5];
-  trit5_digits(v, w);
+__device__ __forceinline__ void build_trit5_bf16(Trit5TablesBf16& tb, int tid, int nthreads) {
+  for (int idx = tid; idx < 256 * kTrit5Copies; idx += nthreads) {
+    int w[5];
+    trit5_digits(idx / kTrit5Copies, w);
 #pragma unroll
-  for (int p = 0; p < 2; ++p) {
-    uint32_t h[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (int p = 0; p < 2; ++p) {
+      uint32_t h[8] = {0, 0, 0, 0, 0, 0, 0, 0};
 #pragma unroll
-    for (int t = 0; t < 5; ++t) h[p + t] = w[t] == 0 ? 0u : (w[t] > 0 ? 0x3F80u : 0xBF80u);
-    tb.t[p][v] = make_uint4(h[0] | h[1] << 16, h[2] | h[3] << 16, h[4] | h[5] << 16, h[6] | h[7] << 16);
+      for (int t = 0; t < 5; ++t) h[p + t] = w[t] == 0 ? 0u : (w[t] > 0 ? 0x3F80u : 0xBF80u);
+      tb.t[p][idx] = make_uint4(h[0] | h[1] << 16, h[2] | h[3] << 16, h[4] | h[5] << 16, h[6] | h[7] << 16);
+    }
   }
 }
 
@@ -220,11 +235,12 @@ __device__ __forceinline__ uint32_t code_byte(const uint32_t (&A)[NA], int i) {
 }
 
 template <int BK, int SEG, bool BF16, bool TABLE>
-__global__ void __launch_bounds__(kBlock) trit5_gemv_kernel(const KernelArgs a) {
+__global__ void __launch_bounds__(fixed_threads(false, BF16, BK)) trit5_gemv_kernel(const KernelArgs a) {
   using Tables = typename std::conditional<BF16, Trit5TablesBf16, Trit5TablesI8>::type;
+  constexpr int WPB = fixed_threads(false, BF16, BK) / kWave;
   __shared__ Tables tab;
   if constexpr (BF16)
-    build_trit5_bf16(tab, threadIdx.x);
+    build_trit5_bf16(tab, threadIdx.x, fixed_threads(false, BF16, BK));
   else
     build_trit5_i8(tab, threadIdx.x);
   __syncthreads();
@@ -235,11 +251,12 @@ __global__ void __launch_bounds__(kBlock) trit5_gemv_kernel(const KernelArgs a) 
   using Acc = typename std::conditional<BF16, float, int>::type;
 
   StepGen<R, TABLE> gen;
-  if (!wave_range(a, gen)) return;
+  if (!wave_range<R, TABLE, WPB>(a, gen)) return;
   const int lane = threadIdx.x & 63;
   const int rho = lane / SEG;
   const int j = lane % SEG;
   const int b0 = j * BK;
+  const int cpy = lane & (kTrit5Copies - 1);
 
   auto load_c = [&](const Step& s, uint32_t (&cw)[ND], uint32_t& o, uint16_t (&SC)[BK]) {
     const auto& g = desc_at<TABLE>(a, s.di);
@@ -325,8 +342,8 @@ __global__ void __launch_bounds__(kBlock) trit5_gemv_kernel(const KernelArgs a) 
       } else {
 #pragma unroll
         for (int c = 0; c < 13; ++c) {
-          const uint4 e0 = tab.t[0][code_byte(A, 26 * t + 2 * c + 0)];
-          const uint4 e1 = tab.t[1][code_byte(A, 26 * t + 2 * c + 1)];
+          const uint4 e0 = tab.t[0][code_byte(A, 26 * t + 2 * c + 0) * kTrit5Copies + cpy];
+          const uint4 e1 = tab.t[1][code_byte(A, 26 * t + 2 * c + 1) * kTrit5Copies + cpy];
           acc = bdot2(e0.x, x[5 * c + 0], acc);
           acc = bdot2(e0.y, x[5 * c + 1], acc);
           acc = bdot2(e0.z | e1.x, x[5 * c + 2], acc);
@@ -347,25 +364,35 @@ __global__ void __launch_bounds__(kBlock) trit5_gemv_kernel(const KernelArgs a) 
 
 // bf16 table: code byte v holds weights k0+b, k0+4+b, k0+8+b, k0+12+b (bit
 // pairs 0..3); entry = those four weights as bf16, pairs (t0,t1), (t2,t3).
+// Kept in kBit2Copies copies (copy c of v at index v * kBit2Copies + c, lane
+// l reads copy l % kBit2Copies): a ds_read_b64 serves 32 lanes at a time;
+// 16 copies (32 KB) leave room for four 256-thread workgroups per CU, which
+// measured faster than 32 conflict-free copies with one 512-thread
+// workgroup.
+constexpr int kBit2Copies = 16;
 struct Bit2TablesBf16 {
-  uint2 t[256];
+  uint2 t[256 * kBit2Copies];
 };
 
-__device__ __forceinline__ void build_bit2_bf16(Bit2TablesBf16& tb, int v) {
-  uint32_t h[4];
+__device__ __forceinline__ void build_bit2_bf16(Bit2TablesBf16& tb, int tid, int nthreads) {
+  for (int idx = tid; idx < 256 * kBit2Copies; idx += nthreads) {
+    const int v = idx / kBit2Copies;
+    uint32_t h[4];
 #pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    int c = (v >> (2 * t)) & 3;
-    h[t] = c == 0 ? 0xBF80u : (c == 2 ? 0x3F80u : 0u);
+    for (int t = 0; t < 4; ++t) {
+      int c = (v >> (2 * t)) & 3;
+      h[t] = c == 0 ? 0xBF80u : (c == 2 ? 0x3F80u : 0u);
+    }
+    tb.t[idx] = make_uint2(h[0] | h[1] << 16, h[2] | h[3] << 16);
   }
-  tb.t[v] = make_uint2(h[0] | h[1] << 16, h[2] | h[3] << 16);
 }
 
 template <int WB, int SEG, bool BF16, bool TABLE>
-__global__ void __launch_bounds__(kBlock) bit2_gemv_kernel(const KernelArgs a) {
-  __shared__ Bit2TablesBf16 tab;
+__global__ void __launch_bounds__(fixed_threads(true, BF16, WB)) bit2_gemv_kernel(const KernelArgs a) {
+  constexpr int WPB = fixed_threads(true, BF16, WB) / kWave;
+  __shared__ typename std::conditional<BF16, Bit2TablesBf16, char>::type tab;
   if constexpr (BF16) {
-    build_bit2_bf16(tab, threadIdx.x);
+    build_bit2_bf16(tab, threadIdx.x, fixed_threads(true, BF16, WB));
     __syncthreads();
   }
 
@@ -376,11 +403,12 @@ __global__ void __launch_bounds__(kBlock) bit2_gemv_kernel(const KernelArgs a) {
   constexpr int NQ = Ends::kNQ;
 
   StepGen<R, TABLE> gen;
-  if (!wave_range(a, gen)) return;
+  if (!wave_range<R, TABLE, WPB>(a, gen)) return;
   const int lane = threadIdx.x & 63;
   const int rho = lane / SEG;
   const int j = lane % SEG;
   const int u0 = j * WB;
+  const int cpy = lane & (kBit2Copies - 1);
   const int ph = Ends::kAligned ? 0 : (u0 & 7);
   const int g0 = u0 >> 3;
 
@@ -479,7 +507,7 @@ __global__ void __launch_bounds__(kBlock) bit2_gemv_kernel(const KernelArgs a) {
       } else {
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
-          const uint2 e = tab.t[(c >> (8 * b)) & 0xFFu];
+          const uint2 e = tab.t[((c >> (8 * b)) & 0xFFu) * kBit2Copies + cpy];
           acc = bdot2(e.x, xr[w][2 * b + 0], acc);
           acc = bdot2(e.y, xr[w][2 * b + 1], acc);
         }

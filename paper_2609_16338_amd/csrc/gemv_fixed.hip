@@ -27,9 +27,10 @@ int launch_fixed(const BatchHeader& h, const GemvDesc* table_dev, const GemvDesc
   a.count = h.count;
   a.pad = 0;
   a.one = one;
-  const int64_t blocks = persistent_blocks(reinterpret_cast<const void*>(fn), h.total_units);
+  const int threads = fixed_k::fixed_threads(h.format == BITCOS_FMT_BIT2, bf16, h.per_lane);
+  const int64_t blocks = persistent_blocks(reinterpret_cast<const void*>(fn), h.total_units, threads);
   if (blocks <= 0 || blocks > 0x7FFFFFFF) return BITCOS_E_HIP;
-  hipLaunchKernelGGL(fn, dim3(static_cast<unsigned>(blocks)), dim3(bitcos_dev::kBlock), 0,
+  hipLaunchKernelGGL(fn, dim3(static_cast<unsigned>(blocks)), dim3(threads), 0,
                      static_cast<hipStream_t>(stream), a);
   return bitcos_launch_status();
 }
