@@ -159,11 +159,37 @@ def sample_rows(n, l, mi, count=SAMPLE_ROWS):
     return np.array(sorted(rows))
 
 
+KSPLIT_MAX = 16384  # longest row a batch-1 tile holds (bf16: 64 lanes x 8 words of 32 weights)
+
+
+def column_blocks(k):
+    """[(k0, width)] of a row of k weights: the whole row, or, for rows longer
+    than KSPLIT_MAX, equal column blocks (a split of K, as row-parallel
+    layers are split across GPUs) whose width is a multiple of 128 that some
+    batch-1 tile covers without idle lanes (the widest such), else the widest
+    multiple of 128 that divides k.  Each block is packed as a matrix of its
+    own; their GEMVs add into one output (the library's _ADD output modes)."""
+    if k <= KSPLIT_MAX:
+        return [(0, k)]
+    cands = [b for b in range(128, KSPLIT_MAX + 1, 128) if k % b == 0]
+    if not cands:
+        return [(0, k)]
+
+    def full(b):
+        words = b // 32
+        return any(words % seg == 0 and words // seg <= 8 for seg in (64, 32, 16, 8, 4))
+    b = max([c for c in cands if full(c)] or cands)
+    return [(k0, b) for k0 in range(0, k, b)]
+
+
 def build_set(wk, layers, fmts, threads, samples=None):
     """Pack every matrix of the layer set in every format (host), upload to HBM.
 
-    With `samples` (a dict), the weights and scales of a few rows of every
-    matrix are kept there, keyed by (layer, matrix), for the self-check."""
+    Entries are (layer, matrix, spec, layout, device blob, (block, k0, width)):
+    one per matrix, or one per column block for rows longer than a batch-1
+    tile (column_blocks).  With `samples` (a dict), the weights and scales of
+    a few rows of every matrix are kept there, keyed by (layer, matrix), for
+    the self-check."""
     import torch
 
     from paper_2609_16338_amd import api
@@ -175,7 +201,12 @@ def build_set(wk, layers, fmts, threads, samples=None):
         w, sc = wl.matrix_inputs(wk.cid, l, mi, spec)
         out = {}
         for fmt in fmts:
-            out[fmt] = api.plan_and_pack(fmt, w, sc, spec.group)
+            out[fmt] = []
+            for c, (k0, kb) in enumerate(column_blocks(spec.k)):
+                wb = np.ascontiguousarray(w[:, k0:k0 + kb])
+                sb = sc.reshape(spec.n, spec.k // 128)[:, k0 // 128:(k0 + kb) // 128] if spec.group == 128 else sc
+                out[fmt].append((api.plan_and_pack(fmt, wb, np.ascontiguousarray(sb).reshape(-1), spec.group),
+                                 (c, k0, kb)))
         keep = None
         if samples is not None:  # (rows, their weights, their fp16 scale bits [rows][k/128] or [1][1])
             rows = sample_rows(spec.n, l, mi)
@@ -186,8 +217,9 @@ def build_set(wk, layers, fmts, threads, samples=None):
     packed = {}
     with cf.ThreadPoolExecutor(max_workers=threads) as ex:
         for (l, mi, spec), out, keep in ex.map(one, jobs):
-            for fmt, (L, blob) in out.items():
-                packed.setdefault(fmt, []).append((l, mi, spec, L, torch.from_numpy(blob).cuda()))
+            for fmt, parts in out.items():
+                for (L, blob), part in parts:
+                    packed.setdefault(fmt, []).append((l, mi, spec, L, torch.from_numpy(blob).cuda(), part))
             if keep is not None:
                 samples[(l, mi)] = keep
     return packed
@@ -241,10 +273,14 @@ def supported(entries, kind, m=1):
 def make_batches(entries, acts, kind):
     """One persistent launch per tile: the step's GEMVs grouped by kernel tile.
 
-    With m activation rows, BITCOS takes all m in one launch (small-batch
-    kernel); the five-trit and 2-bit layouts, which have no small-batch
-    kernel, take m batch-1 launches per tile, one per activation row, as
-    their m > 1 entry points do."""
+    Column blocks of a long row (column_blocks) go to phases: every matrix's
+    first block (and every unsplit matrix) in phase 0, which writes the
+    outputs; block c in phase c, whose launches add onto them (_ADD output
+    mode) after the launches of phase c - 1 on the same stream, so each
+    output is a deterministic sum.  With m activation rows, BITCOS takes all
+    m in one launch (small-batch kernel); the five-trit and 2-bit layouts,
+    which have no small-batch kernel, take m batch-1 launches per tile, one
+    per activation row, as their m > 1 entry points do."""
     import torch
 
     from paper_2609_16338_amd import _native as N
@@ -256,22 +292,45 @@ def make_batches(entries, acts, kind):
     groups = {}
     for e in entries:
         info = api.describe(e[3], rows_per_launch, xd)
-        groups.setdefault((info.kernel, info.per_lane, info.seg_lanes), []).append(e)
+        groups.setdefault((e[5][0], info.kernel, info.per_lane, info.seg_lanes), []).append(e)
+    ys = {}
+    for e in entries:
+        if (e[0], e[1]) not in ys:
+            ys[(e[0], e[1])] = torch.empty((m, e[2].n), dtype=torch.float32, device="cuda")
+    # Activations of a block: a contiguous copy of its columns (made once).
+    blk = {}
+
+    def x_of(e):
+        c, k0, kb = e[5]
+        x, a = acts[(kind, e[2].k)]
+        if kb == e[2].k:
+            return x, a
+        key = (e[2].k, k0, kb)
+        if key not in blk:
+            blk[key] = (x[:, k0:k0 + kb].contiguous(),
+                        None if a is None else a[:, k0 // 128:(k0 + kb) // 128].contiguous())
+        return blk[key]
+
     batches = []
-    for tile, ents in sorted(groups.items(), key=lambda kv: -sum(e[3].n * e[3].k for e in kv[1])):
-        ys = [torch.empty((m, e[3].n), dtype=torch.float32, device="cuda") for e in ents]
+    order = sorted(groups.items(), key=lambda kv: (kv[0][0], -sum(e[3].n * e[3].k for e in kv[1])))
+    for key, ents in order:
+        phase = key[0]
+        outs = [ys[(e[0], e[1])] for e in ents]
         for r0 in range(0, m, rows_per_launch):
             r1 = r0 + rows_per_launch
-            xs = [acts[(kind, e[2].k)][0][r0:r1] for e in ents]  # [rows, k]: the batch takes rows from its shape
+            xs = [x_of(e)[0][r0:r1] for e in ents]  # [rows, k]: the batch takes rows from its shape
             xs = [x.reshape(-1) if rows_per_launch == 1 else x for x in xs]
-            xss = [acts[(kind, e[2].k)][1] for e in ents]
+            xss = [x_of(e)[1] for e in ents]
             xss = [None if v is None else v[r0:r1].reshape(-1) for v in xss]
-            b = api.Batch([e[3] for e in ents], [e[4] for e in ents], xs, [y[r0:r1].reshape(-1) for y in ys],
-                          xss if any(v is not None for v in xss) else None)
-            b.tile = tile[1:]
-            b.kernel = tile[0]
+            b = api.Batch([e[3] for e in ents], [e[4] for e in ents], xs, [y[r0:r1].reshape(-1) for y in outs],
+                          xss if any(v is not None for v in xss) else None,
+                          y_mode=N.Y_F32 if phase == 0 else N.Y_F32_ADD)
+            b.tile = key[2:]
+            b.kernel = key[1]
+            b.phase = phase
             b.entries = ents
-            b.outputs = ys
+            b.outputs = outs
+            b.keep_x = blk
             batches.append(b)
     return batches
 
@@ -354,7 +413,7 @@ def device_copies(entries, copies):
     """The layer set and copies - 1 clones of its device blobs (same layouts)."""
     sets = [entries]
     for _ in range(copies - 1):
-        sets.append([(l, mi, spec, L, blob.clone()) for (l, mi, spec, L, blob) in entries])
+        sets.append([(l, mi, spec, L, blob.clone(), part) for (l, mi, spec, L, blob, part) in entries])
     return sets
 
 
@@ -427,9 +486,13 @@ def check_outputs(batches, samples, xhost, kind):
     import torch
     torch.cuda.synchronize()
     ok, rows_checked, worst = True, 0, 0.0
+    seen = set()
     for b in batches:
         for e, y in zip(b.entries, b.outputs):
             l, mi, spec = e[0], e[1], e[2]
+            if (l, mi) in seen:  # the column blocks of a matrix share its output
+                continue
+            seen.add((l, mi))
             rows, w_rows, s_rows = samples[(l, mi)]
             x, xs = xhost[(kind, spec.k)]
             ref, kbar, gbar = dense_rows(w_rows, s_rows, spec.group, x, xs)
@@ -910,6 +973,9 @@ def main(argv=None):
             "global_batch": m,
             "layers": layers,
             "gemvs_per_step": len(packed[N.FMT_BITCOS]),
+            "matrices_per_step": len({(e[0], e[1]) for e in packed[N.FMT_BITCOS]}),
+            "column_blocks": {f"{s.name} {s.n}x{s.k}": len(column_blocks(s.k)) for s in wk.matrices
+                              if len(column_blocks(s.k)) > 1},
             "weights_per_step": weights,
             "payload_bytes_per_step": int(r["payload"][N.FMT_BITCOS]),
             "total_bytes_per_step": int(r["total"][N.FMT_BITCOS]

@@ -93,6 +93,13 @@ extern "C" {
 
 #define BITCOS_Y_F32 1        /* y float32 [m][N], scaled                 */
 #define BITCOS_Y_I32_RAW 2    /* y int32 [m][N] = sum_k W x, unscaled (int8 x only) */
+/* Accumulating forms of the two: the result is added onto what y already
+ * holds (y += ...), e.g. to sum the partial products of a matrix stored as
+ * column blocks (a split of K: block c holds columns [c Kc, (c+1) Kc) as a
+ * matrix of its own).  Every output element is added once per call, so calls
+ * that follow one another on a stream add in that order (deterministic). */
+#define BITCOS_Y_F32_ADD 3
+#define BITCOS_Y_I32_RAW_ADD 4
 
 /* Plain-old-data description of one packed matrix.  Filled by *_plan();
  * passed by pointer to pack/unpack/gemv.  Section offsets are relative to the
@@ -156,7 +163,8 @@ int bitcos_unpack(const bitcos_layout* L, const void* blob, size_t blob_bytes, i
  *   xscale_dev  NULL (a = 1) or device fp32 [m][k/128] per-group activation
  *             scales a (int8 activations quantised per group of 128).
  *   y_dev     device output [m][n], overwritten: fp32 (BITCOS_Y_F32) or the
- *             unscaled int32 row sums (BITCOS_Y_I32_RAW, int8 x only, exact).
+ *             unscaled int32 row sums (BITCOS_Y_I32_RAW, int8 x only, exact);
+ *             or added onto (BITCOS_Y_F32_ADD, BITCOS_Y_I32_RAW_ADD).
  * int8 x accumulates exactly in int32 per group and applies the scale once per
  * group in fp32; with one scale per tensor and no xscale the full int32 row
  * sum is multiplied once.  bf16 x accumulates in fp32.

@@ -23,7 +23,7 @@ FMT_BITCOS, FMT_TRIT5, FMT_BIT2 = 1, 2, 3
 SEC_BITMAP, SEC_SIGNS, SEC_OFFSETS, SEC_SCALES = 0, 1, 2, 3
 SEC_CODES = 0
 X_I8, X_BF16 = 1, 2
-Y_F32, Y_I32_RAW = 1, 2
+Y_F32, Y_I32_RAW, Y_F32_ADD, Y_I32_RAW_ADD = 1, 2, 3, 4
 MAX_M = 16  # most activation rows per GEMV call
 NOALLOC_MAX_ROWS = 262144  # rows bitcos_pack_device_noalloc's fixed workspace holds
 KERNEL_GENERAL, KERNEL_STREAMING, KERNEL_MATRIX, KERNEL_SMALL_BATCH, KERNEL_FIXED = 1, 2, 3, 4, 5

@@ -15,7 +15,7 @@ import numpy as np
 
 from . import _native as N
 from ._native import (FMT_BIT2, FMT_BITCOS, FMT_TRIT5, LaunchInfo, Layout, X_BF16, X_I8,  # noqa: F401
-                      Y_F32, Y_I32_RAW)
+                      Y_F32, Y_F32_ADD, Y_I32_RAW, Y_I32_RAW_ADD)
 
 
 def _ptr(a: np.ndarray) -> ctypes.c_void_p:
@@ -193,8 +193,9 @@ def gemv(L: Layout, blob_dev, x, y, xscale=None, y_mode: int = Y_F32, stream=Non
     """Enqueue y = (S (.) W) x for the layout's format on `stream`.
 
     blob_dev: uint8 cuda tensor of >= L.total_bytes; x: int8 or bfloat16 cuda
-    tensor [m, k] (or [k]); y: float32 (Y_F32) or int32 (Y_I32_RAW) cuda
-    tensor [m, n] (or [n]); xscale: None or float32 cuda tensor [m, k/128].
+    tensor [m, k] (or [k]); y: float32 (Y_F32, Y_F32_ADD) or int32 (Y_I32_RAW,
+    Y_I32_RAW_ADD) cuda tensor [m, n] (or [n]), overwritten or (the _ADD modes)
+    added onto; xscale: None or float32 cuda tensor [m, k/128].
     """
     import torch
     m = x.shape[0] if x.dim() == 2 else 1
@@ -211,7 +212,7 @@ def gemv(L: Layout, blob_dev, x, y, xscale=None, y_mode: int = Y_F32, stream=Non
         raise ValueError("blob_dev must be uint8 with at least total_bytes elements")
     if x.numel() != m * L.k:
         raise ValueError("x has the wrong size")
-    want_y = torch.int32 if y_mode == Y_I32_RAW else torch.float32
+    want_y = torch.int32 if y_mode in (Y_I32_RAW, Y_I32_RAW_ADD) else torch.float32
     if y.dtype != want_y or y.numel() != m * L.n:
         raise ValueError("y has the wrong dtype or size")
     xs_ptr = None
@@ -317,7 +318,7 @@ def _check_gemv_buffers(L, blob_dev, x, y, xscale, y_mode, m=1):
         raise ValueError("blob_dev must be uint8 with at least total_bytes elements")
     if x.numel() != m * L.k or x.dtype not in (torch.int8, torch.bfloat16):
         raise ValueError("x must be int8 or bfloat16 with m * k elements")
-    want_y = torch.int32 if y_mode == Y_I32_RAW else torch.float32
+    want_y = torch.int32 if y_mode in (Y_I32_RAW, Y_I32_RAW_ADD) else torch.float32
     if y.dtype != want_y or y.numel() != m * L.n:
         raise ValueError("y has the wrong dtype or size")
 

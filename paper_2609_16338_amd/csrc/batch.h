@@ -44,6 +44,7 @@ static_assert(sizeof(GemvDesc) == 128, "GemvDesc is 128 bytes");
 constexpr int kModeGrouped = 1;  // one scale per (row, 128-group)
 constexpr int kModeXscale = 2;   // per-group activation scales
 constexpr int kModeRaw = 4;      // int32 raw row sums
+constexpr int kModeAdd = 8;      // add the result onto y instead of overwriting it
 
 constexpr uint32_t kBatchMagic = 0x42435342u;  // "BSCB"
 

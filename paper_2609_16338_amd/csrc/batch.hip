@@ -52,8 +52,11 @@ int make_desc(const bitcos_layout* L, const void* blob_dev, const void* x_dev, c
   int st = check_layout(L);
   if (st) return st;
   if (x_dtype != BITCOS_X_I8 && x_dtype != BITCOS_X_BF16) return BITCOS_E_ARG;
-  if (y_mode != BITCOS_Y_F32 && y_mode != BITCOS_Y_I32_RAW) return BITCOS_E_ARG;
-  if (y_mode == BITCOS_Y_I32_RAW && x_dtype != BITCOS_X_I8) return BITCOS_E_ARG;
+  if (y_mode != BITCOS_Y_F32 && y_mode != BITCOS_Y_I32_RAW && y_mode != BITCOS_Y_F32_ADD &&
+      y_mode != BITCOS_Y_I32_RAW_ADD)
+    return BITCOS_E_ARG;
+  const bool raw_y = y_mode == BITCOS_Y_I32_RAW || y_mode == BITCOS_Y_I32_RAW_ADD;
+  if (raw_y && x_dtype != BITCOS_X_I8) return BITCOS_E_ARG;
   if (!blob_dev || !x_dev || !y_dev) return BITCOS_E_ARG;
   if (xscale_dev && L->k % 128) return BITCOS_E_ARG;
   int per_lane = 0, seg = 0, rows = 0;
@@ -80,7 +83,8 @@ int make_desc(const bitcos_layout* L, const void* blob_dev, const void* x_dev, c
   d->x_bytes = static_cast<uint32_t>(xb);
   d->y_bytes = static_cast<uint32_t>(yb);
   d->mode = (L->group == 128 ? kModeGrouped : 0) | (xscale_dev ? kModeXscale : 0) |
-            (y_mode == BITCOS_Y_I32_RAW ? kModeRaw : 0);
+            (raw_y ? kModeRaw : 0) |
+            (y_mode == BITCOS_Y_F32_ADD || y_mode == BITCOS_Y_I32_RAW_ADD ? kModeAdd : 0);
   if (L->format == BITCOS_FMT_BITCOS) {
     d->signs = reinterpret_cast<const uint32_t*>(blob + L->sec_off[BITCOS_SEC_SIGNS]);
     d->signs_bytes = static_cast<uint32_t>(L->sec_bytes[BITCOS_SEC_SIGNS]);

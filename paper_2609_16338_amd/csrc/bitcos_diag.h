@@ -433,9 +433,10 @@ __global__ void __launch_bounds__(diag_threads(W, BF16)) bitcos_diag_kernel(cons
   // its wait (so that wait never waits on the store).
   bool pend = false;
   uint32_t pend_bits = 0, pend_voff = 0, pend_soff = kOOB;
+  int pend_mode = 0;
   rsrc_t pend_ry = ry;
   auto flush_store = [&] {
-    if (pend) __builtin_amdgcn_raw_buffer_store_b32(pend_bits, pend_ry, pend_voff, pend_soff, 0);
+    if (pend) put_y(pend_bits, pend_ry, pend_voff, pend_soff, (pend_mode & kModeAdd) != 0, (pend_mode & kModeRaw) != 0);
     pend = false;
   };
 
@@ -558,6 +559,7 @@ __global__ void __launch_bounds__(diag_threads(W, BF16)) bitcos_diag_kernel(cons
     pend_bits = bits;
     pend_voff = 4u * static_cast<uint32_t>(row);
     pend_soff = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(s.row0) * 4u);
+    pend_mode = mode;
     pend_ry = ry;
   };
 

@@ -241,9 +241,10 @@ __global__ void __launch_bounds__(fast_threads(W, BF16)) bitcos_fast_kernel(cons
   // its wait (so that wait never waits on the store).
   bool pend = false;
   uint32_t pend_bits = 0, pend_soff = kOOB;
+  int pend_mode = 0;
   rsrc_t pend_ry = ry;
   auto flush_store = [&] {
-    if (pend) __builtin_amdgcn_raw_buffer_store_b32(pend_bits, pend_ry, voff_y, pend_soff, 0);
+    if (pend) put_y(pend_bits, pend_ry, voff_y, pend_soff, (pend_mode & kModeAdd) != 0, (pend_mode & kModeRaw) != 0);
     pend = false;
   };
 
@@ -358,6 +359,7 @@ __global__ void __launch_bounds__(fast_threads(W, BF16)) bitcos_fast_kernel(cons
       pend = j == SEG - 1;
       pend_bits = static_cast<uint32_t>(tot);
       pend_soff = soff_y;
+      pend_mode = mode;
       pend_ry = ry;
       return;
     }
@@ -384,6 +386,7 @@ __global__ void __launch_bounds__(fast_threads(W, BF16)) bitcos_fast_kernel(cons
     pend = j == SEG - 1;
     pend_bits = __builtin_bit_cast(uint32_t, part);
     pend_soff = soff_y;
+    pend_mode = mode;
     pend_ry = ry;
   };
 

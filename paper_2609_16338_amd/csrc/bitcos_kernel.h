@@ -54,6 +54,7 @@ using bitcos::GemvDesc;
 using bitcos::kModeGrouped;
 using bitcos::kModeRaw;
 using bitcos::kModeXscale;
+using bitcos::kModeAdd;
 
 struct KernelArgs {
   const GemvDesc* __restrict__ table;  // batch: descriptor table in device memory
@@ -420,6 +421,7 @@ __global__ void __launch_bounds__(Cfg<BF16>::kThreads) bitcos_gemv_kernel(const 
   float tensor_scale = 0.0f;
   int mode = 0;
   void* ydst = nullptr;
+  uint32_t ybytes = 0;
 
   Step s1 = gen.next(a);
   uint32_t P1[W], lo1[W], hi1[W], sh1[W];
@@ -473,6 +475,7 @@ __global__ void __launch_bounds__(Cfg<BF16>::kThreads) bitcos_gemv_kernel(const 
       }
       tensor_scale = half_bits_to_float(gp_u16(g.scales)[0]);
       ydst = g.y;
+      ybytes = g.y_bytes;
     }
 
     const int row = s0.row0 + rho;
@@ -491,7 +494,8 @@ __global__ void __launch_bounds__(Cfg<BF16>::kThreads) bitcos_gemv_kernel(const 
 
     if (!BF16 && (mode & kModeRaw)) {
       const int tot = seg_sum<SEG>(static_cast<int>(run[W - 1]));
-      if (j == SEG - 1 && live) gp_i32_out(ydst)[row] = tot;
+      if (j == SEG - 1 && live)
+        put_y(static_cast<uint32_t>(tot), make_rsrc(ydst, ybytes), 4u * row, 0, (mode & kModeAdd) != 0, true);
       continue;
     }
     float part;
@@ -515,7 +519,8 @@ __global__ void __launch_bounds__(Cfg<BF16>::kThreads) bitcos_gemv_kernel(const 
       }
       part = seg_sum<SEG>(BF16 ? 2.0f * f : f);
     }
-    if (j == SEG - 1 && live) gp_f32_out(ydst)[row] = part;
+    if (j == SEG - 1 && live)
+      put_y(__builtin_bit_cast(uint32_t, part), make_rsrc(ydst, ybytes), 4u * row, 0, (mode & kModeAdd) != 0, false);
   }
 }
 

@@ -224,7 +224,7 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
   // ---- decode side: output of the GEMV whose step is being decoded
   int ddi = -1, dn = 0;
   // scaled: per-group fp32 accumulation; dxs: the GEMV has activation scales
-  bool grouped = false, raw = false, scaled = false, dxs = false;
+  bool grouped = false, raw = false, scaled = false, dxs = false, dadd = false;
   float tscale = 0.0f;
   rsrc_t ry = make_rsrc(nullptr, 0);
 
@@ -263,6 +263,7 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
       dn = D.n;
       grouped = (D.mode & kModeGrouped) != 0;
       raw = !BF16 && (D.mode & kModeRaw);
+      dadd = (D.mode & kModeAdd) != 0;
       dxs = XS && (D.mode & kModeXscale);
       scaled = !raw && (grouped || dxs);
       tscale = half_bits_to_float(gp_u16(D.scales)[0]);
@@ -409,7 +410,7 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
           else
             f = tscale * static_cast<float>(iacc[r][i]);
           const uint32_t bits = raw ? static_cast<uint32_t>(iacc[r][i]) : __builtin_bit_cast(uint32_t, f);
-          __builtin_amdgcn_raw_buffer_store_b32(bits, ry, off, 0, 0);
+          put_y(bits, ry, off, 0, dadd, raw);
           acc[r][i] = 0.0f;
           iacc[r][i] = 0;
         }

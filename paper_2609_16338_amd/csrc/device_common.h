@@ -49,6 +49,20 @@ __device__ __forceinline__ uint16_t ld16(rsrc_t r, uint32_t off) {
   return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
 }
 
+// One output element through a buffer resource (dropped past its range): a
+// store, or with `add` an atomic add onto what y holds (fp32; int32 for raw
+// sums).  A launch writes each element once, so the additions of launches
+// that follow one another on a stream happen in that order and the result
+// is deterministic.
+__device__ __forceinline__ void put_y(uint32_t bits, rsrc_t r, uint32_t voff, uint32_t soff, bool add, bool raw) {
+  if (!add)
+    __builtin_amdgcn_raw_buffer_store_b32(bits, r, voff, soff, 0);
+  else if (raw)
+    __builtin_amdgcn_raw_ptr_buffer_atomic_add_i32(static_cast<int>(bits), r, voff, soff, 0);
+  else
+    __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(__builtin_bit_cast(float, bits), r, voff, soff, 0);
+}
+
 // Waits until every vector-memory access of the wave has completed: vmcnt 0,
 // the LDS/scalar and export counts untouched (s_waitcnt immediate 0x0F70 on
 // gfx9).  Issued through the builtin rather than inline asm so that the

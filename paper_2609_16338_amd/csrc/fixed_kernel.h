@@ -33,6 +33,7 @@ using bitcos::GemvDesc;
 using bitcos::kModeGrouped;
 using bitcos::kModeRaw;
 using bitcos::kModeXscale;
+using bitcos::kModeAdd;
 
 struct KernelArgs {
   const GemvDesc* __restrict__ table;  // batch: descriptor table in device memory
@@ -109,13 +110,14 @@ __device__ __forceinline__ bool wave_range(const KernelArgs& a, StepGen<R, TABLE
 // Common epilogue: reduce the lane partials of one row and store.  SC holds
 // the row's group scales for the lane's groups (fp16 bits, grouped mode).
 template <int SEG, bool BF16, int PER, int UPG, class Acc>
-__device__ __forceinline__ void finish_row(int mode, void* ydst, const Acc (&run)[PER], int row,
+__device__ __forceinline__ void finish_row(int mode, void* ydst, uint32_t ybytes, const Acc (&run)[PER], int row,
                                            bool live, int j, int ph, const float* xs,
                                            const uint16_t* SC, float tensor_scale) {
   using Ends = GroupEnds<PER, UPG>;
+  const bool add = (mode & kModeAdd) != 0;
   if (!BF16 && (mode & kModeRaw)) {
     const int tot = seg_sum<SEG>(static_cast<int>(run[PER - 1]));
-    if (j == SEG - 1 && live) gp_i32_out(ydst)[row] = tot;
+    if (j == SEG - 1 && live) put_y(static_cast<uint32_t>(tot), make_rsrc(ydst, ybytes), 4u * row, 0, add, true);
     return;
   }
   float part;
@@ -138,7 +140,7 @@ __device__ __forceinline__ void finish_row(int mode, void* ydst, const Acc (&run
     }
     part = seg_sum<SEG>(f);
   }
-  if (j == SEG - 1 && live) gp_f32_out(ydst)[row] = part;
+  if (j == SEG - 1 && live) put_y(__builtin_bit_cast(uint32_t, part), make_rsrc(ydst, ybytes), 4u * row, 0, add, false);
 }
 
 // The lane's group scales for one row (grouped mode), else zeros.
@@ -278,6 +280,7 @@ __global__ void __launch_bounds__(fixed_threads(false, BF16, BK)) trit5_gemv_ker
   float tensor_scale = 0.0f;
   int mode = 0;
   void* ydst = nullptr;
+  uint32_t ybytes = 0;
 
   Step s1 = gen.next(a);
   uint32_t cw1[ND], o1;
@@ -306,6 +309,7 @@ __global__ void __launch_bounds__(fixed_threads(false, BF16, BK)) trit5_gemv_ker
       tensor_scale = half_bits_to_float(gp_u16(g.scales)[0]);
       mode = g.mode;
       ydst = g.y;
+      ybytes = g.y_bytes;
       wait_vmem_all();
     }
     // The next step's loads, issued after the activations of a GEMV the wave
@@ -354,7 +358,7 @@ __global__ void __launch_bounds__(fixed_threads(false, BF16, BK)) trit5_gemv_ker
       run[t] = acc;
     }
     __builtin_amdgcn_s_setprio(0);
-    finish_row<SEG, BF16, BK, 1>(mode, ydst, run, row, live, j, 0, xs, SC0, tensor_scale);
+    finish_row<SEG, BF16, BK, 1>(mode, ydst, ybytes, run, row, live, j, 0, xs, SC0, tensor_scale);
   }
 }
 
@@ -437,6 +441,7 @@ __global__ void __launch_bounds__(fixed_threads(true, BF16, WB)) bit2_gemv_kerne
   float tensor_scale = 0.0f;
   int mode = 0;
   void* ydst = nullptr;
+  uint32_t ybytes = 0;
 
   Step s1 = gen.next(a);
   uint32_t cw1[WB];
@@ -482,6 +487,7 @@ __global__ void __launch_bounds__(fixed_threads(true, BF16, WB)) bit2_gemv_kerne
       tensor_scale = half_bits_to_float(gp_u16(g.scales)[0]);
       mode = g.mode;
       ydst = g.y;
+      ybytes = g.y_bytes;
       wait_vmem_all();
     }
     // The next step's loads, issued after the activations of a GEMV the wave
@@ -515,7 +521,7 @@ __global__ void __launch_bounds__(fixed_threads(true, BF16, WB)) bit2_gemv_kerne
       run[w] = acc;
     }
     __builtin_amdgcn_s_setprio(0);
-    finish_row<SEG, BF16, WB, 8>(mode, ydst, run, row, live, j, ph, xs, SC0, tensor_scale);
+    finish_row<SEG, BF16, WB, 8>(mode, ydst, ybytes, run, row, live, j, ph, xs, SC0, tensor_scale);
   }
 }
 

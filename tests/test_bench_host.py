@@ -63,13 +63,14 @@ def test_device_copies_share_layouts_and_clone_blobs():
         def clone(self):
             return Blob(self.tag + "'")
 
-    entries = [(0, 1, "spec", "L0", Blob("b0")), (1, 2, "spec", "L1", Blob("b1"))]
+    entries = [(0, 1, "spec", "L0", Blob("b0"), (0, 0, 8)), (1, 2, "spec", "L1", Blob("b1"), (1, 8, 8))]
     sets = bench.device_copies(entries, 3)
     assert len(sets) == 3 and sets[0] is entries
     for st in sets[1:]:
         assert [e[3] for e in st] == ["L0", "L1"]
         assert [e[4].tag for e in st] == ["b0'", "b1'"]
         assert all(a[4] is not b[4] for a, b in zip(st, entries))
+        assert [e[5] for e in st] == [(0, 0, 8), (1, 8, 8)]
 
 
 def test_supported_reports_baselines_without_a_long_row_kernel():
@@ -86,7 +87,7 @@ def test_supported_reports_baselines_without_a_long_row_kernel():
     sc = np.full((3, k // 128), 0.01, np.float16)
     for fmt, bf16_ok in ((N.FMT_BITCOS, True), (N.FMT_TRIT5, False), (N.FMT_BIT2, False)):
         L, _ = api.plan_and_pack(fmt, w, sc, 128)
-        entries = [(0, 6, None, L, None)]
+        entries = [(0, 6, None, L, None, (0, 0, k))]
         assert bench.supported(entries, "bf16", 1) is bf16_ok
         assert bench.supported(entries, "int8", 1)
         assert bench.supported(entries, "bf16", 4) is bf16_ok  # baselines at m > 1: batch-1 launches
@@ -143,3 +144,14 @@ def test_self_check_reference_matches_the_oracle(group, kind):
         bound = group_bound(w[rows], sc if group == 0 else sbits.reshape(-1), group, q, a)
         assert np.allclose(gbar, bound, rtol=1e-12)
     assert np.array_equal(y.astype(np.float32), ref)
+
+
+def test_column_blocks_split_only_long_rows():
+    assert bench.column_blocks(5120) == [(0, 5120)]
+    assert bench.column_blocks(16384) == [(0, 16384)]
+    # the Qwen3-32B-like down projection: five blocks of the hidden size
+    assert bench.column_blocks(25600) == [(k0, 5120) for k0 in range(0, 25600, 5120)]
+    for k in (16512, 20480, 32768, 49152):
+        blocks = bench.column_blocks(k)
+        assert sum(b for _, b in blocks) == k and all(b % 128 == 0 and b <= bench.KSPLIT_MAX for _, b in blocks)
+        assert [k0 for k0, _ in blocks] == list(range(0, k, blocks[0][1]))

@@ -154,7 +154,10 @@ def test_bitnet_step_as_timed(bitnet_set, fmt, kind):
 @pytest.fixture(scope="module")
 def qwen32_set():
     wk = wl.WORKLOADS["qwen3_32b_layers"]
-    layers = 4  # every launch of the batch-1 and M = 16 steps exceeds twice the resident waves
+    # Every launch of the batch-1 and M = 16 steps exceeds twice the resident
+    # waves: the smallest are the phases that add the down projections' later
+    # column blocks (five-trit int8: 8-row steps, layers x 640 units).
+    layers = 26
     samples = {}
     say("building the Qwen3-32B-like set:", layers, "layers, 3 formats")
     packed = bench.build_set(wk, layers, FMTS, 16, samples)
