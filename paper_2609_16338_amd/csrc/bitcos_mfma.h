@@ -16,14 +16,16 @@
 //     32-weight word g = l / 16, so the four lane groups of a row cover one
 //     group together and an MFMA never mixes two scale groups.
 //   * B operand (weights, K x 16 rows): per presence byte of the lane's word
-//     the 8 weights come out of two LDS table lookups keyed by the presence
-//     byte m and the next 8 compact sign bits s, combined by v_perm_b32
-//     (Eq. (2) w = p - 2n, with the deposit of Sec. II-B done by the table):
-//     int8 +-1 bytes for v_mfma_i32_16x16x64_i8, bf16 +-0.5 for
+//     the 8 weights come out of two LDS table lookups (tables.h) keyed by the
+//     presence byte m and the next 8 compact sign bits s, combined by
+//     v_perm_b32 (Eq. (2) w = p - 2n, with the deposit of Sec. II-B done by
+//     the table): int8 +-1 bytes for v_mfma_i32_16x16x64_i8, bf16 +-0.5 for
 //     v_mfma_f32_16x16x32_bf16 (the 0.5 is undone exactly at the end).
 //   * A operand (activations, 16 batch rows x K): lane (m, g) holds batch row
 //     m's activations at the positions its B partner decodes; rows m >= M
 //     read zero through the buffer range check, so one kernel serves every M.
+//     Loaded directly, or (staged) in whole 16-byte pieces per batch row and
+//     handed to the lanes through a per-wave LDS transpose buffer.
 //   * C (16 batch rows x 16 output rows): lane l holds batch rows
 //     4 (l / 16) + i of output row l % 16.  Every group's C is scaled into
 //     fp32 accumulators (fp16 group scale x activation scale, Sec. II-C), or
@@ -37,10 +39,13 @@
 // issued at the start of step t (the sign range of step t+1 follows from the
 // popcounts of step t).  Activations of step t+1 are issued during step t,
 // group by group as step t's MFMAs release their registers, so that waiting
-// for them never waits on a prefetch issued after them.
+// for them never waits on a prefetch issued after them.  Inside a step the
+// table lookups of group q + 1 are in flight while group q's weights are
+// built and multiplied, and the two tiles' MFMA chains alternate.
 #pragma once
 
 #include "mfma_common.h"
+#include "tables.h"
 
 namespace bitcos_k {
 
@@ -48,16 +53,41 @@ constexpr int kMfmaTile = 16;                   // output rows per MFMA tile
 constexpr int kMfmaRT = 2;                      // tiles per work unit
 constexpr int kMfmaRows = kMfmaTile * kMfmaRT;  // rows per work unit
 // Workgroup size: one workgroup per CU (the decode tables fill most of the
-// LDS).  int8: 3 waves per SIMD (within 168 registers, no spills), measured
-// 12-18 % faster than 2 on the Qwen3-32B-like layers at M = 4 and 16.  bf16:
-// 2 waves per SIMD; at 3 it fits without activation scales but ran 4-5 %
-// slower, and with them it spills.  Host and device both use it.
+// LDS), 2 waves per SIMD: the group lookahead below holds about 240
+// registers (bf16).  int8 at 3 waves per SIMD and without the lookahead
+// spills with activation scales and measured slower.  Host and device both
+// use it.
 constexpr int mfma_threads(bool bf16, bool xs) {
+  (void)bf16;
   (void)xs;
-  return bf16 ? 512 : 768;
+  return 512;
 }
 constexpr int kMfmaMaxBatch = 16;
-constexpr int kSignStride = 21;                 // LDS dwords per staged row (20 used; odd spreads banks)
+constexpr int kSignStride = 21;  // LDS dwords per staged sign row (20 used; odd spreads banks)
+// The table lookups of group q + 1 are issued before group q's arithmetic.
+constexpr bool mfma_lookahead(bool bf16) {
+  (void)bf16;
+  return true;
+}
+// Activation loads.  Direct: lane (m, g) reads batch row m at its word (16
+// bytes per load, every load touching 16 rows x 2 cache lines).  Staged:
+// each load reads whole 16-byte pieces of a few batch rows in order (fully
+// used lines) and the wave's transpose buffer in LDS hands every lane its
+// MFMA operand; it adds an LDS round trip per group but touches a quarter of
+// the lines.  On 8 Qwen3-32B-like layers (us per step, bf16 / int8): direct
+// 595 / 721 at M = 4 and 840 / 781 at M = 16; staged 714 / 706 at M = 4 and
+// 719 / 714 at M = 16.
+constexpr int mfma_xrow(bool bf16) { return (bf16 ? 256 : 128) + 16; }  // one group's activations of a batch row, padded
+constexpr int mfma_xbuf_bytes(bool bf16, bool stage) { return stage ? 16 * mfma_xrow(bf16) : 16; }
+constexpr bool mfma_staged(int m, bool bf16) { return !bf16 || m > 8; }
+// Sign-table copies (tables.h): 32 when the tables and the waves' sign
+// stages fit the LDS, else 16.
+constexpr int mfma_sign_copies(bool bf16, bool stage) {
+  return 65536 + 2048 * 32 + (mfma_threads(bf16, false) / 64) * (kMfmaRows * kSignStride * 4 + mfma_xbuf_bytes(bf16, stage)) <=
+                 kLdsBytes
+             ? 32
+             : 16;
+}
 
 // Wave-uniform position of one step.
 struct MStep {
@@ -68,9 +98,9 @@ struct MStep {
   bool valid;
 };
 
-template <bool BF16, bool XS, bool TABLE>
+template <bool BF16, bool XS, bool TABLE, bool STAGE>
 __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(const KernelArgs a) {
-  constexpr int NC = Cfg<BF16>::kCopies;
+  constexpr int CT = mfma_sign_copies(BF16, STAGE);
   constexpr int THREADS = mfma_threads(BF16, XS);
   constexpr int WPB = THREADS / kWave;
   constexpr int RT = kMfmaRT;
@@ -78,9 +108,11 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
   constexpr int NA = BF16 ? 4 : 2;    // MFMAs (16-byte activation pieces) per word
   using CV = typename std::conditional<BF16, f32x4_t, i32x4_t>::type;
 
-  __shared__ typename MfmaTables<BF16>::type tab;
+  __shared__ FastTables<BF16, CT> tab;
   __shared__ uint32_t sstage[WPB * kMfmaRows * kSignStride];
-  build_mfma_tables(tab, threadIdx.x, THREADS);
+  __shared__ uint4 xbufs[WPB * mfma_xbuf_bytes(BF16, STAGE) / 16];
+  static_assert(sizeof(tab) + sizeof(sstage) + sizeof(xbufs) <= kLdsBytes, "small-batch kernel LDS");
+  build_fast_tables<BF16, CT>(tab, threadIdx.x, THREADS);
   __syncthreads();
 
   const int lane = threadIdx.x & 63;
@@ -96,8 +128,11 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
 
   const int nr = lane & 15;
   const int g = lane >> 4;
-  const int cp = lane & (NC - 1);
+  const FastLane fl = fast_lane<BF16, CT>(lane);
   uint32_t* const stage = sstage + wv * (kMfmaRows * kSignStride);
+  uint8_t* const xbuf = reinterpret_cast<uint8_t*>(xbufs) + wv * mfma_xbuf_bytes(BF16, STAGE);
+  constexpr int XROW = mfma_xrow(BF16);
+  constexpr int XLR = BF16 ? 16 : 8;  // lanes per batch row in a coalesced load (16-byte pieces)
 
   // ---- fetch side: the GEMV whose step is being fetched; fbeg / fend: its
   // first step in the launch and one past its last, fC: steps per unit.
@@ -194,9 +229,21 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
   auto issue_x = [&](const MStep& s, int q) {
     const int gi = 4 * (s.valid ? s.c : 0) + q;
     const bool ok = s.valid && gi < fG;
-    const uint32_t off = ok ? (static_cast<uint32_t>(nr * fk) + 128u * gi + 32u * g) * ELEM : kOOB;
+    if constexpr (STAGE) {
+      // Coalesced: load jj covers batch rows XLR/4... of the group, each row's
+      // 128 activations as contiguous 16-byte pieces (lane l: row
+      // (64 / XLR) jj + l / XLR, piece l % XLR).
 #pragma unroll
-    for (int j = 0; j < NA; ++j) A[q][j] = ld128(rx, off + 16u * j);
+      for (int jj = 0; jj < NA; ++jj) {
+        const uint32_t row = static_cast<uint32_t>((64 / XLR) * jj + lane / XLR);
+        const uint32_t off = ok ? (row * fk + 128u * gi) * ELEM + 16u * static_cast<uint32_t>(lane % XLR) : kOOB;
+        A[q][jj] = ld128(rx, off);
+      }
+    } else {
+      const uint32_t off = ok ? (static_cast<uint32_t>(nr * fk) + 128u * gi + 32u * g) * ELEM : kOOB;
+#pragma unroll
+      for (int j = 0; j < NA; ++j) A[q][j] = ld128(rx, off + 16u * j);
+    }
     if constexpr (XS) {
 #pragma unroll
       for (int i = 0; i < 4; ++i)
@@ -338,49 +385,79 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
         }
       }
     };
+    // Table lookups of a group: per tile, the lane's word and its 64-bit
+    // sign window from the staged block.  bf16 looks group 0 up here and, in
+    // group q, group q + 1 while q's weights are built and multiplied; int8
+    // looks each group up where it is used.  The two tiles' MFMA chains
+    // alternate so consecutive MFMAs do not depend on each other.
+    auto lookup1 = [&](int q, int r) {
+      const uint32_t* srow = stage + (kMfmaTile * r + nr) * kSignStride;
+      const uint32_t bpos = rel[r][q];
+      const uint32_t S = __builtin_amdgcn_alignbit(srow[(bpos >> 5) + 1], srow[bpos >> 5], bpos);
+      return fast_look<BF16, CT>(cur.P[r][q], S, tab, fl);
+    };
+    // The MFMAs of one tile's word: (bf16) 4 MFMAs of 8 weights, (int8) 2 of
+    // 16, each weight dword perm(T[s], E[m]).
+    auto mfma_word = [&](const Look<BF16>& L, const u32x4_t (&Aq)[NA], int j, CV c) {
+      if constexpr (BF16) {
+        const uint2 th = L.th[j];
+        const uint4 sb = L.sb[j];
+        const u32x4_t w = {__builtin_amdgcn_perm(th.y, th.x, sb.x), __builtin_amdgcn_perm(th.y, th.x, sb.y),
+                           __builtin_amdgcn_perm(th.y, th.x, sb.z), __builtin_amdgcn_perm(th.y, th.x, sb.w)};
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, Aq[j]),
+                                                       __builtin_bit_cast(bf16x8_t, w), c, 0, 0, 0);
+      } else {
+        const uint2 t0 = L.tv[2 * j], e0 = L.sv[2 * j];
+        const uint2 t1 = L.tv[2 * j + 1], e1 = L.sv[2 * j + 1];
+        const u32x4_t w = {__builtin_amdgcn_perm(t0.y, t0.x, e0.x), __builtin_amdgcn_perm(t0.y, t0.x, e0.y),
+                           __builtin_amdgcn_perm(t1.y, t1.x, e1.x), __builtin_amdgcn_perm(t1.y, t1.x, e1.y)};
+        return __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4_t, Aq[j]),
+                                                     __builtin_bit_cast(i32x4_t, w), c, 0, 0, 0);
+      }
+    };
+    constexpr bool LA = mfma_lookahead(BF16);
+    Look<BF16> lk[2][RT];
+    if constexpr (LA) {
+#pragma unroll
+      for (int r = 0; r < RT; ++r) lk[0][r] = lookup1(0, r);
+    }
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
+      if (LA && q + 1 < 4) {
 #pragma unroll
-      for (int r = 0; r < RT; ++r) {
-        const uint32_t* srow = stage + (kMfmaTile * r + nr) * kSignStride;
-        const uint32_t bpos = rel[r][q];
-        const uint32_t S = __builtin_amdgcn_alignbit(srow[(bpos >> 5) + 1], srow[bpos >> 5], bpos);
-        const uint32_t Pw = cur.P[r][q];
-        CV c = CV{0, 0, 0, 0};
-        uint32_t rr = 0;
-        if constexpr (BF16) {
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const uint32_t m = __builtin_amdgcn_ubfe(Pw, 8 * j, 8);
-            const uint32_t s = __builtin_amdgcn_ubfe(S, rr, 8);
-            rr = __builtin_popcount(m) + rr;
-            const uint4 sb = tab.selb[m * NC + cp];
-            const uint2 th = tab.tsh[s * NC + cp];
-            const u32x4_t w = {__builtin_amdgcn_perm(th.y, th.x, sb.x), __builtin_amdgcn_perm(th.y, th.x, sb.y),
-                               __builtin_amdgcn_perm(th.y, th.x, sb.z), __builtin_amdgcn_perm(th.y, th.x, sb.w)};
-            c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, A[q][j]),
-                                                        __builtin_bit_cast(bf16x8_t, w), c, 0, 0, 0);
-          }
-        } else {
-          uint2 wb[4];
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const uint32_t m = __builtin_amdgcn_ubfe(Pw, 8 * j, 8);
-            const uint32_t s = __builtin_amdgcn_ubfe(S, rr, 8);
-            rr = __builtin_popcount(m) + rr;
-            const uint2 ex = tab.exp[m * NC + cp];
-            const uint2 tg = tab.tsg[s * NC + cp];
-            wb[j] = make_uint2(__builtin_amdgcn_perm(tg.y, tg.x, ex.x), __builtin_amdgcn_perm(tg.y, tg.x, ex.y));
-          }
-#pragma unroll
-          for (int j = 0; j < 2; ++j) {
-            const u32x4_t w = {wb[2 * j].x, wb[2 * j].y, wb[2 * j + 1].x, wb[2 * j + 1].y};
-            c = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4_t, A[q][j]),
-                                                      __builtin_bit_cast(i32x4_t, w), c, 0, 0, 0);
-          }
-        }
-        cg[q & 1][r] = c;
+        for (int r = 0; r < RT; ++r) lk[(q + 1) & 1][r] = lookup1(q + 1, r);
       }
+      // The group's activations in MFMA order: lane (nr, g) takes batch row
+      // nr at its word's pieces (staged: through the wave's transpose buffer).
+      u32x4_t Aq[NA];
+      if constexpr (STAGE) {
+#pragma unroll
+        for (int jj = 0; jj < NA; ++jj)
+          *reinterpret_cast<u32x4_t*>(xbuf + ((64 / XLR) * jj + lane / XLR) * XROW + 16 * (lane % XLR)) = A[q][jj];
+#pragma unroll
+        for (int j = 0; j < NA; ++j) Aq[j] = *reinterpret_cast<const u32x4_t*>(xbuf + nr * XROW + 16 * (NA * g + j));
+      } else {
+#pragma unroll
+        for (int j = 0; j < NA; ++j) Aq[j] = A[q][j];
+      }
+      CV c[RT];
+#pragma unroll
+      for (int r = 0; r < RT; ++r) c[r] = CV{0, 0, 0, 0};
+      if constexpr (LA) {  // the two tiles' chains alternate
+#pragma unroll
+        for (int j = 0; j < NA; ++j)
+#pragma unroll
+          for (int r = 0; r < RT; ++r) c[r] = mfma_word(lk[q & 1][r], Aq, j, c[r]);
+      } else {  // one tile's lookups live at a time
+#pragma unroll
+        for (int r = 0; r < RT; ++r) {
+          const Look<BF16> L = lookup1(q, r);
+#pragma unroll
+          for (int j = 0; j < NA; ++j) c[r] = mfma_word(L, Aq, j, c[r]);
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < RT; ++r) cg[q & 1][r] = c[r];
       // This group's activations are consumed: fetch step t+1's.
       float xa_q[4];
 #pragma unroll
@@ -422,13 +499,15 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
 
 using MfmaFn = void (*)(const KernelArgs);
 
-inline MfmaFn pick_mfma(bool bf16, bool xs, bool table) {
-  if (bf16) {
-    if (xs) return table ? bitcos_mfma_kernel<true, true, true> : bitcos_mfma_kernel<true, true, false>;
-    return table ? bitcos_mfma_kernel<true, false, true> : bitcos_mfma_kernel<true, false, false>;
-  }
-  if (xs) return table ? bitcos_mfma_kernel<false, true, true> : bitcos_mfma_kernel<false, true, false>;
-  return table ? bitcos_mfma_kernel<false, false, true> : bitcos_mfma_kernel<false, false, false>;
+template <bool BF16, bool XS>
+MfmaFn pick_mfma_t(bool table, bool stage) {
+  if (stage) return table ? bitcos_mfma_kernel<BF16, XS, true, true> : bitcos_mfma_kernel<BF16, XS, false, true>;
+  return table ? bitcos_mfma_kernel<BF16, XS, true, false> : bitcos_mfma_kernel<BF16, XS, false, false>;
+}
+
+inline MfmaFn pick_mfma(bool bf16, bool xs, bool table, bool stage) {
+  if (bf16) return xs ? pick_mfma_t<true, true>(table, stage) : pick_mfma_t<true, false>(table, stage);
+  return xs ? pick_mfma_t<false, true>(table, stage) : pick_mfma_t<false, false>(table, stage);
 }
 
 }  // namespace bitcos_k
