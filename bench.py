@@ -113,7 +113,7 @@ def emit(obj, args):
 
 # Sources of the BITCOS kernels: a stored HBM-traffic measurement is reported
 # only while these files are unchanged.
-KERNEL_SOURCES = ["bitcos_diag.h", "bitcos_fast.h", "bitcos_kernel.h", "bitcos_mfma.h", "mfma_common.h",
+KERNEL_SOURCES = ["bitcos_diag.h", "bitcos_fast.h", "bitcos_kernel.h", "bitcos_mfma.h", "mfma_common.h", "tables.h",
                   "device_common.h", "batch.h", "batch.hip", "gemv_bitcos.hip", "launch_common.h", "plan.h"]
 TRAFFIC_FILES = {
     "qwen3_32b_layers": os.path.join(ROOT, "profiles", "bitcos_fast_bf16_qwen3_32b_k5120_traffic.txt"),
@@ -737,7 +737,7 @@ def profile_pass(args):
     wk = wl.WORKLOADS[args.workload]
     layers = args.layers or wk.layers
     packed = build_set(wk, layers, [N.FMT_BITCOS], args.threads)
-    acts, _ = activations(wk, ("bf16",))
+    acts, _ = activations(wk, ("bf16",), args.batch)
     top = make_batches(packed[N.FMT_BITCOS], acts, "bf16")[0]
     for _ in range(5):
         top.run()
@@ -748,7 +748,7 @@ def profile_pass(args):
     for _ in range(5):
         dst.copy_(src)
     torch.cuda.synchronize()
-    alg = sum(e[3].payload_bits / 8 + e[3].k * 2 + e[3].n * 4 for e in top.entries)
+    alg = sum(e[3].payload_bits / 8 + args.batch * (e[3].k * 2 + e[3].n * 4) for e in top.entries)
     print(f"[profile-pass] {args.workload} dominant launch: {len(top.entries)} GEMVs, tile {top.tile}, "
           f"algorithmic bytes {int(alg)}; copy {COPY_MIB} MiB; kernel_source_hash {kernel_source_hash()}",
           flush=True)

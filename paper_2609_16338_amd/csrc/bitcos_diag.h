@@ -36,6 +36,7 @@
 
 #include "bitcos_fast.h"
 #include "mfma_common.h"
+#include "tables.h"
 
 namespace bitcos_k {
 
@@ -111,29 +112,9 @@ __device__ __forceinline__ T diag_row_sum(T c0, T c1, T c2, T c3, int lane, bool
   }
 }
 
-// Decode tables of the diag kernel, in deposit form (see mfma_common.h):
-// E[m] turns compact values into position order, T[s] holds the compact
-// values.  Each entry is kept in several copies, copy c of entry e at index
-// e * copies + c, and lane l reads copy l % copies.  On gfx950 a ds_read_b64
-// serves 32 lanes at a time from 64 banks, so 32 copies of an 8-byte entry
-// keep any 32 keys on distinct banks (16 copies see about 1.7x the cycles of
-// a conflict-free read); a ds_read_b128 serves 16 lanes, for which 16 copies
-// suffice.  CT is the sign table's copy count.
-template <bool BF16, int CT>
-struct DiagTables;
-template <int CT>
-struct DiagTables<false, CT> {
-  static constexpr int kCopiesE = 16, kCopiesT = CT;
-  uint2 e[256 * kCopiesE];
-  uint2 t[256 * kCopiesT];
-};
-template <int CT>
-struct DiagTables<true, CT> {
-  static constexpr int kCopiesE = 16, kCopiesT = CT;
-  uint4 e[256 * kCopiesE];
-  uint2 t[256 * kCopiesT];
-};
-
+// Decode tables: the deposit-form tables of tables.h (E[m] turns compact
+// values into position order, T[s] holds the compact values), addressed by
+// one v_perm_b32 per lookup.
 // Workgroup size of the diag kernel: one workgroup per CU with as many waves
 // per SIMD as the tile's registers allow without spilling (bf16 tiles hold
 // the next word's lookups too).  Host and device both use it.
@@ -142,101 +123,39 @@ constexpr int diag_waves_per_simd(int w, bool bf16) {
 }
 constexpr int diag_threads(int w, bool bf16) { return 256 * diag_waves_per_simd(w, bf16); }
 
-// Sign-table copies of the diag kernel for (words per lane, bf16?).
-// 32 sign-table copies (conflict-free) measured no faster than 16 on the
-// BitNet-like set; 16 leave LDS to spare.
+// Sign-table copies of the diag kernel for (words per lane, bf16?): 16
+// (32, conflict-free, measured no faster on the BitNet-like set), or 8 when
+// 16 do not fit beside the stage buffers (int8, 16 words per lane).
+constexpr int diag_sign_dwords(int w) { return 64 * w + 4; }
 constexpr int diag_sign_copies(int w, bool bf16) {
-  (void)w;
-  (void)bf16;
-  return 16;
+  return 65536 + 2048 * 16 + 2 * (diag_threads(w, bf16) / 64) * diag_sign_dwords(w) * 4 <= kLdsBytes ? 16 : 8;
 }
 
 // Prefetch ring depth: loads one step ahead.  Two steps ahead (with the
 // third sign buffer paid for by 16-copy sign tables) measured no faster on
 // the BitNet-like set: the decode, not the HBM latency, bounds the kernel.
-constexpr int diag_sign_dwords(int w) { return 64 * w + 4; }
 constexpr int diag_stages(int w, bool bf16) {
   (void)w;
   (void)bf16;
   return 2;
 }
 
-template <bool BF16, int CT>
-__device__ __forceinline__ void build_diag_tables(DiagTables<BF16, CT>& tab, int tid, int nthreads) {
-  using Tb = DiagTables<BF16, CT>;
-  constexpr int NE = 256 * Tb::kCopiesE, NT = 256 * Tb::kCopiesT;
-  for (int idx = tid; idx < NE + NT; idx += nthreads) {
-    const bool sign = idx >= NE;
-    const int e = sign ? (idx - NE) / Tb::kCopiesT : idx / Tb::kCopiesE;
-    uint32_t rank[8], val[8];
-    uint32_t r = 0;
-#pragma unroll
-    for (int b = 0; b < 8; ++b) {
-      const bool on = (e >> b) & 1;
-      rank[b] = on ? r : 0x0Cu;  // v_perm_b32 selector 0x0C writes 0
-      r += on;
-      val[b] = on ? (BF16 ? 0xBFu : 0xFFu) : (BF16 ? 0x3Fu : 0x01u);
-    }
-    if (sign) {
-      tab.t[idx - NE] = make_uint2(bytes4(val[0], val[1], val[2], val[3]), bytes4(val[4], val[5], val[6], val[7]));
-    } else if constexpr (BF16) {  // bf16 output b: low byte 0, high byte the rank's value
-      tab.e[idx] = make_uint4(bytes4(0x0C, rank[0], 0x0C, rank[1]), bytes4(0x0C, rank[2], 0x0C, rank[3]),
-                              bytes4(0x0C, rank[4], 0x0C, rank[5]), bytes4(0x0C, rank[6], 0x0C, rank[7]));
-    } else {
-      tab.e[idx] = make_uint2(bytes4(rank[0], rank[1], rank[2], rank[3]), bytes4(rank[4], rank[5], rank[6], rank[7]));
-    }
-  }
-}
-
-// Table lookups of one 32-weight word in deposit form: per presence byte m
-// and its next 8 compact signs s, E[m] (position -> rank selectors) and T[s]
-// (the +-1 values, or the high bytes of +-0.5 bf16, in compact order).
-template <bool BF16>
-struct DiagLook;
-template <>
-struct DiagLook<false> {
-  uint2 e[4];
-  uint2 t[4];
-};
-template <>
-struct DiagLook<true> {
-  uint4 e[4];
-  uint2 t[4];
-};
-
-template <bool BF16, int CT>
-__device__ __forceinline__ DiagLook<BF16> diag_look(uint32_t P, uint32_t S, const DiagTables<BF16, CT>& tab, int lane) {
-  using Tb = DiagTables<BF16, CT>;
-  const int ce = lane & (Tb::kCopiesE - 1), ct = lane & (Tb::kCopiesT - 1);
-  DiagLook<BF16> L;
-  uint32_t r = 0;
-#pragma unroll
-  for (int b = 0; b < 4; ++b) {
-    const uint32_t m = __builtin_amdgcn_ubfe(P, 8 * b, 8);
-    const uint32_t s = __builtin_amdgcn_ubfe(S, r, 8);
-    if (b < 3) r = __builtin_popcount(m) + r;
-    L.e[b] = tab.e[m * Tb::kCopiesE + ce];
-    L.t[b] = tab.t[s * Tb::kCopiesT + ct];
-  }
-  return L;
-}
-
 // The word's weights (perm) multiplied against its activations x (32 bf16 in
 // 16 dwords or 32 int8 in 8) on the matrix cores, into two accumulators.
 template <bool BF16, class CV>
-__device__ __forceinline__ void diag_math(const DiagLook<BF16>& L, const uint32_t* x, CV (&c)[2]) {
+__device__ __forceinline__ void diag_math(const Look<BF16>& L, const uint32_t* x, CV (&c)[2]) {
 #pragma unroll
   for (int b = 0; b < 4; ++b) {
     if constexpr (BF16) {
-      const uint2 t = L.t[b];
-      const uint4 e = L.e[b];
+      const uint2 t = L.th[b];
+      const uint4 e = L.sb[b];
       const u32x4_t wt = {__builtin_amdgcn_perm(t.y, t.x, e.x), __builtin_amdgcn_perm(t.y, t.x, e.y),
                           __builtin_amdgcn_perm(t.y, t.x, e.z), __builtin_amdgcn_perm(t.y, t.x, e.w)};
       const u32x4_t xv = {x[4 * b], x[4 * b + 1], x[4 * b + 2], x[4 * b + 3]};
       c[b & 1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, xv),
                                                          __builtin_bit_cast(bf16x8_t, wt), c[b & 1], 0, 0, 0);
     } else if (b & 1) {
-      const uint2 t0 = L.t[b - 1], e0 = L.e[b - 1], t1 = L.t[b], e1 = L.e[b];
+      const uint2 t0 = L.tv[b - 1], e0 = L.sv[b - 1], t1 = L.tv[b], e1 = L.sv[b];
       const u32x4_t wt = {__builtin_amdgcn_perm(t0.y, t0.x, e0.x), __builtin_amdgcn_perm(t0.y, t0.x, e0.y),
                           __builtin_amdgcn_perm(t1.y, t1.x, e1.x), __builtin_amdgcn_perm(t1.y, t1.x, e1.y)};
       const int h = b >> 1;
@@ -305,11 +224,13 @@ __global__ void __launch_bounds__(diag_threads(W, BF16)) bitcos_diag_kernel(cons
   using Acc = typename std::conditional<BF16, float, int>::type;
   using CV = typename std::conditional<BF16, f32x4_t, i32x4_t>::type;
 
-  __shared__ DiagTables<BF16, diag_sign_copies(W, BF16)> tab;
+  constexpr int CT = diag_sign_copies(W, BF16);
+  __shared__ FastTables<BF16, CT> tab;
   __shared__ uint4 sbuf0[WPB * SCR / 4];
   __shared__ uint4 sbuf1[WPB * SCR / 4];
   __shared__ uint4 sbuf2[D > 2 ? WPB * SCR / 4 : 1];
-  build_diag_tables(tab, threadIdx.x, diag_threads(W, BF16));
+  static_assert(sizeof(tab) + 2 * sizeof(sbuf0) <= kLdsBytes, "diag kernel LDS");
+  build_fast_tables<BF16, CT>(tab, threadIdx.x, diag_threads(W, BF16));
   __syncthreads();
 
   const int lane = threadIdx.x & 63;
@@ -321,6 +242,7 @@ __global__ void __launch_bounds__(diag_threads(W, BF16)) bitcos_diag_kernel(cons
   const int U0 = per * wave;
   const int U1 = min(U0 + per, total);
   if (U0 >= U1) return;
+  const FastLane fl = fast_lane<BF16, CT>(lane);
 
   // Lane layout: i = lane % 16 picks the row, the q group a quarter of its segments.
   const int i16 = lane & 15;
@@ -527,17 +449,17 @@ __global__ void __launch_bounds__(diag_threads(W, BF16)) bitcos_diag_kernel(cons
     // (except on the widest int8 tiles, whose registers go to activations).
     CV acc[2] = {CV{0, 0, 0, 0}, CV{0, 0, 0, 0}};
     if constexpr (BF16 || W <= 12) {
-      DiagLook<BF16> L = diag_look(Pw[0], S[0], tab, lane);
+      Look<BF16> L = fast_look<BF16, CT>(Pw[0], S[0], tab, fl);
 #pragma unroll
       for (int w = 0; w < W; ++w) {
-        DiagLook<BF16> Ln;
-        if (w + 1 < W) Ln = diag_look(Pw[w + 1], S[w + 1], tab, lane);
+        Look<BF16> Ln;
+        if (w + 1 < W) Ln = fast_look<BF16, CT>(Pw[w + 1], S[w + 1], tab, fl);
         diag_math<BF16>(L, xr[w], acc);
         if (w + 1 < W) L = Ln;
       }
     } else {
 #pragma unroll
-      for (int w = 0; w < W; ++w) diag_math<BF16>(diag_look(Pw[w], S[w], tab, lane), xr[w], acc);
+      for (int w = 0; w < W; ++w) diag_math<BF16>(fast_look<BF16, CT>(Pw[w], S[w], tab, fl), xr[w], acc);
     }
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_s_setprio(0);
