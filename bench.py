@@ -92,6 +92,8 @@ def parse(argv=None):
     ap.add_argument("--out", default="", help="also write the JSON line to this file")
     ap.add_argument("--profile-pass", action="store_true",
                     help="for counter runs: the dominant BITCOS launch x5, then a plain 256 MiB device copy x5")
+    ap.add_argument("--profile-sweep", action="store_true",
+                    help="for counter runs: the z = 0.42 sweep launch of every format, int8 and bf16, x5 each")
     ap.add_argument("--sweep", action="store_true",
                     help="zero-density sweep on one 8192 x 8192 matrix: BITCOS vs five-trit vs 2-bit (own JSON line)")
     ap.add_argument("--gamma", action="store_true",
@@ -657,7 +659,11 @@ def dominant_roofline(r, args, name):
              N.KERNEL_GENERAL: "bitcos_gemv_kernel", N.KERNEL_SMALL_BATCH: "bitcos_mfma_kernel",
              }.get(kinds.pop(), "?") if len(kinds) == 1 else "mixed"
     return {
+        # The roofline the metric is read against (weight bytes per second vs
+        # HBM peak); what limits the kernel today is the larger two_term term,
+        # restated as "limiter".
         "bound": "hbm",
+        "limiter": "instructions" if launch_gamma > hbm_term else "hbm",
         "achieved": round(achieved, 2),
         "peak": HBM_PEAK_GBS,
         "unit": "GB/s",
@@ -752,6 +758,43 @@ def profile_pass(args):
     print(f"[profile-pass] {args.workload} dominant launch: {len(top.entries)} GEMVs, tile {top.tile}, "
           f"algorithmic bytes {int(alg)}; copy {COPY_MIB} MiB; kernel_source_hash {kernel_source_hash()}",
           flush=True)
+
+
+def profile_sweep(args):
+    """Counter runs on the zero-density sweep's launch at z = 0.42 (one 8192 x
+    8192 g128 matrix, --sweep-copies device copies in one launch): BITCOS,
+    five-trit and 2-bit, int8 then bf16 activations, each launch 5 times."""
+    import torch
+
+    from paper_2609_16338_amd import _native as N
+    from paper_2609_16338_amd import api
+
+    cid, k, z = 4, 8192, 0.42
+    zi = wl.SWEEP_Z.index(z)
+    spec = wl.sweep_spec(z)
+    w, sc = wl.matrix_inputs(cid, 0, zi, spec)
+    xi = torch.from_numpy(wl.activation_inputs(cid, "int8", 1, k)).cuda().reshape(-1)
+    xb = torch.from_numpy(wl.activation_inputs(cid, "bf16", 1, k).view(np.int16)).view(torch.bfloat16).cuda().reshape(-1)
+    for fmt in (N.FMT_BITCOS, N.FMT_TRIT5, N.FMT_BIT2):
+        L, blob = api.plan_and_pack(fmt, w, sc, spec.group)
+        src = torch.from_numpy(blob).cuda()
+        blobs = [src.clone() for _ in range(args.sweep_copies)]
+        for kind, x in (("int8", xi), ("bf16", xb)):
+            ys = [torch.empty(spec.n, dtype=torch.float32, device="cuda") for _ in blobs]
+            b = api.Batch([L] * len(blobs), blobs, [x] * len(blobs), ys)
+            for _ in range(5):
+                b.run()
+            torch.cuda.synchronize()
+            try:
+                d = api.describe(L, 1, N.X_I8 if kind == "int8" else N.X_BF16)
+                tile = f"kernel {d.kernel}, tile ({d.per_lane}, {d.seg_lanes})"
+            except N.BitcosError:
+                tile = "tile n/a"
+            print(f"[profile-sweep] {FMT_NAMES[fmt]} {kind}: {len(blobs)} GEMVs of {spec.n}x{spec.k}, {tile}, "
+                  f"payload bytes per GEMV {L.payload_bits // 8}", flush=True)
+            del b, ys
+        del blobs, src
+        torch.cuda.empty_cache()
 
 
 def hbm_read(args):
@@ -929,6 +972,9 @@ def main(argv=None):
         return
     if args.profile_pass:
         profile_pass(args)
+        return
+    if args.profile_sweep:
+        profile_sweep(args)
         return
     if args.sweep:
         sweep(args)
