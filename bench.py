@@ -133,9 +133,12 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def stored_traffic(workload):
+def stored_traffic(workload, kernel):
     """HBM bytes per launch of the dominant kernel from the FETCH_SIZE / WRITE_SIZE
-    passes (scaled by the copy calibration), or None if the kernel changed since."""
+    passes (scaled by the copy calibration), or None if the kernel changed since
+    or the stored launch is another kernel or tile than `kernel` (say
+    "bitcos_fast_kernel<5, 32,": a small-batch run of the same set launches
+    a different kernel)."""
     path = TRAFFIC_FILES.get(workload)
     try:
         with open(path) as f:
@@ -144,6 +147,8 @@ def stored_traffic(workload):
         return None
     kv = {k.strip(): v.strip() for k, v in kv.items()}
     if kv.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    if kernel not in kv.get("kernel", ""):
         return None
     try:
         return int(float(kv["traffic_bytes_per_launch"]))
@@ -668,7 +673,7 @@ def dominant_roofline(r, args, name):
         "peak": HBM_PEAK_GBS,
         "unit": "GB/s",
         "frac": round(achieved / HBM_PEAK_GBS, 4),
-        "traffic": stored_traffic(name),
+        "traffic": stored_traffic(name, f"{kname}<{top.tile[0]}, {top.tile[1]},"),
         "kernel": f"{kname}<{top.tile[0]},{top.tile[1]},bf16,table>: {len(top.entries)} GEMVs in one launch",
         "per_launch_us": round(per_launch_us, 3),
         "bytes_per_launch": int(alg_bytes),

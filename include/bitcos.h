@@ -137,14 +137,19 @@ int bitcos_plan(const int8_t* w, int32_t n, int32_t k, int32_t group, int32_t un
  * patterns, [n][k/128] or [1]; finite and non-negative) into host memory
  * dst of `cap` bytes (>= L->total_bytes).  Bytes are a deterministic
  * function of (W, scales, *L); padding is zero.  Errors: E_ARG, E_VALUE
- * (bad weight or scale, W not the one planned), E_SPACE. */
+ * (bad weight or scale, W not the one planned), E_SPACE.  Paper: Sec. II-A
+ * (a presence bit per weight, a sign bit per non-zero in the same row-major
+ * order, 2 - z bits per weight by Eq. (1)); the fp16 scale per 128-weight
+ * group is the deployed models' convention of Sec. I and Table I. */
 int bitcos_pack(const int8_t* w, const uint16_t* scales_f16, const bitcos_layout* L, void* dst,
                 size_t cap);
 
 /* bitcos_unpack: exact inverse of bitcos_pack on a host blob of
  * `blob_bytes` bytes: writes W (host int8 [n][k]) and the scales (host
  * fp16 bits).  Verifies the bitmap popcount against nnz and every unit
- * offset; E_VALUE on a mismatch. */
+ * offset; E_VALUE on a mismatch.  Paper: Sec. II-A and Fig. 1 (the j-th
+ * stored sign belongs to the j-th set bit of the bitmap); the weight is
+ * w = p - 2n of Eq. (2), Sec. II-C. */
 int bitcos_unpack(const bitcos_layout* L, const void* blob, size_t blob_bytes, int8_t* w_out,
                   uint16_t* scales_out);
 
@@ -169,7 +174,11 @@ int bitcos_unpack(const bitcos_layout* L, const void* blob, size_t blob_bytes, i
  * group in fp32; with one scale per tensor and no xscale the full int32 row
  * sum is multiplied once.  bf16 x accumulates in fp32.
  * Errors: E_ARG (also m outside 1..BITCOS_MAX_M), E_UNSUPPORTED (dtype or
- * shape without a kernel), E_HIP. */
+ * shape without a kernel), E_HIP.  Paper: Sec. II-C (ternary weights
+ * w = p - 2n, Eq. (2), contracted against int8 activations into int32 with
+ * the group scale applied once per group) and Sec. II-B / II-D (the same
+ * contraction with floating-point activations); the GEMV of a decode step,
+ * Sec. III. */
 int bitcos_gemv(const bitcos_layout* L, const void* blob_dev, int32_t m, const void* x_dev,
                 int32_t x_dtype, const float* xscale_dev, void* y_dev, int32_t y_mode,
                 void* stream);

@@ -155,3 +155,17 @@ def test_column_blocks_split_only_long_rows():
         blocks = bench.column_blocks(k)
         assert sum(b for _, b in blocks) == k and all(b % 128 == 0 and b <= bench.KSPLIT_MAX for _, b in blocks)
         assert [k0 for k0, _ in blocks] == list(range(0, k, blocks[0][1]))
+
+
+def test_stored_traffic_only_for_the_measured_kernel_and_tile():
+    """A stored FETCH/WRITE measurement belongs to one kernel and tile: a run
+    of the same layer set on another kernel (the small-batch one at M > 1)
+    must report traffic as unmeasured, not borrow the batch-1 figure."""
+    with open(bench.TRAFFIC_FILES["qwen3_32b_layers"]) as f:
+        kernel = next(line.split(":", 1)[1].strip() for line in f if line.startswith("kernel:"))
+    measured = kernel.split("::")[-1].split("<")[0]
+    tile = kernel.split("<")[1].split(",")[:2]
+    other = "bitcos_mfma_kernel" if measured != "bitcos_mfma_kernel" else "bitcos_fast_kernel"
+    assert bench.stored_traffic("qwen3_32b_layers", f"{other}<{tile[0]},{tile[1]},") is None
+    assert bench.stored_traffic("qwen3_32b_layers", f"{measured}<{int(tile[0]) + 1}, {tile[1].strip()},") is None
+    assert bench.stored_traffic("no_such_set", f"{measured}<") is None
