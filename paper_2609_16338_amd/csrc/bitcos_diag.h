@@ -53,16 +53,6 @@ __device__ __forceinline__ T qperm(T v) {
   return bits_as<T>(__builtin_amdgcn_update_dpp(0, as_bits(v), CTRL, 0xF, 0xF, false));
 }
 
-// A per-lane all-ones / all-zeros mask the compiler cannot see through.
-// Conditions on cross-lane results are applied with these masks instead of
-// selects: a select may be turned into a branch around the DPP or permlane
-// move, which then runs with lanes switched off and reads them as zero.
-__device__ __forceinline__ uint32_t lane_mask(bool on) {
-  uint32_t m = on ? ~0u : 0u;
-  asm volatile("" : "+v"(m));
-  return m;
-}
-
 // Row sums of the diagonal elements.  Lane 16 (i/4) + i holds element i in
 // accumulator register i % 4, so in every quad on the diagonal (lanes 20a ..
 // 20a + 3) lane 20a + t holds register t.  Returns the row's total in the lane
@@ -397,7 +387,11 @@ __global__ void __launch_bounds__(diag_threads(W, BF16)) bitcos_diag_kernel(cons
       wait_vmem_all();
     }
     next();
-    const uint32_t* scr32 = reinterpret_cast<const uint32_t*>(stage_buf(stage_c));
+    // LDS byte address of the stage buffer, in bits (cursors below count from
+    // LDS address 0, so a window's dword address is one shift and mask).
+    using LdsU32 = const __attribute__((address_space(3))) uint32_t;
+    const uint32_t stage_bits =
+        static_cast<uint32_t>(reinterpret_cast<size_t>((LdsU32*)stage_buf(stage_c))) * 8u + wave_bits;
     if (ragged) {
 #pragma unroll
       for (int w = 0; w < W; ++w)
@@ -417,13 +411,13 @@ __global__ void __launch_bounds__(diag_threads(W, BF16)) bitcos_diag_kernel(cons
     // q groups per row, an exclusive prefix in row-major (row, segment) order.
     uint32_t base;
     if constexpr (kRowOffsets) {
-      base = wave_bits + (ROFF[k] - (s.off0 & ~31u)) + static_cast<uint32_t>(row_prefix<S4>(cnt, pbits));
+      base = stage_bits + (ROFF[k] - (s.off0 & ~31u)) + static_cast<uint32_t>(row_prefix<S4>(cnt, pbits));
     } else if constexpr (SEG == 64) {
-      base = wave_bits + (s.off0 & 31u) + static_cast<uint32_t>(wave_incl_scan(cnt) - cnt);
+      base = stage_bits + (s.off0 & 31u) + static_cast<uint32_t>(wave_incl_scan(cnt) - cnt);
     } else {
       const int nc = __builtin_amdgcn_ds_bpermute(src_addr, cnt);
       const int excl = __builtin_amdgcn_ds_bpermute(nat_addr, wave_incl_scan(nc) - nc);
-      base = wave_bits + (s.off0 & 31u) + static_cast<uint32_t>(excl);
+      base = stage_bits + (s.off0 & 31u) + static_cast<uint32_t>(excl);
     }
     __builtin_amdgcn_wave_barrier();
     // The windows, lookups and multiplies of the step at raised wave
@@ -437,11 +431,11 @@ __global__ void __launch_bounds__(diag_threads(W, BF16)) bitcos_diag_kernel(cons
     // clamped once so that every window stays in the wave's own buffer (a
     // valid cursor never needs it; a word's offset in the lane is < 32 W).
     uint32_t S[W];
-    const uint32_t bclamp = min(base, wave_bits + (SCR - 2 - W) * 32u);
+    const uint32_t bclamp = min(base, stage_bits + (SCR - 2 - W) * 32u);
 #pragma unroll
     for (int w = 0; w < W; ++w) {
       const uint32_t b = bclamp + static_cast<uint32_t>(pc[w]);
-      const uint32_t* sp = scr32 + (b >> 5);
+      LdsU32* sp = (LdsU32*)static_cast<size_t>((b >> 3) & ~3u);
       S[w] = __builtin_amdgcn_alignbit(sp[1], sp[0], b);
     }
     // Two accumulators, alternating, so consecutive MFMAs do not wait on each

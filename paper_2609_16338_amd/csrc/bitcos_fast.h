@@ -159,8 +159,7 @@ __global__ void __launch_bounds__(fast_threads(W, BF16)) bitcos_fast_kernel(cons
     else if constexpr (k == 1) return sbuf1;
     else return sbuf2;
   };
-  // Sign-bit cursors count from the start of a stage buffer, so a word's
-  // window dword is just cursor / 32.
+  // Offset of the wave's part of a stage buffer, in bits.
   const uint32_t wave_bits = static_cast<uint32_t>(wv) * SCR * 32u;
 
   FastGen<R, TABLE> gen;
@@ -306,7 +305,11 @@ __global__ void __launch_bounds__(fast_threads(W, BF16)) bitcos_fast_kernel(cons
       wait_vmem_all();
     }
     next();
-    const uint32_t* scr32 = reinterpret_cast<const uint32_t*>(stage_buf(stage_c));
+    // LDS byte address of the stage buffer, in bits, so a window's dword
+    // address is one shift and mask of its bit cursor.
+    using LdsU32 = const __attribute__((address_space(3))) uint32_t;
+    const uint32_t stage_bits =
+        static_cast<uint32_t>(reinterpret_cast<size_t>((LdsU32*)stage_buf(stage_c))) * 8u;
     // Words past the end of a row (ragged tiles only) count as empty.
     if (ragged) {
 #pragma unroll
@@ -323,7 +326,7 @@ __global__ void __launch_bounds__(fast_threads(W, BF16)) bitcos_fast_kernel(cons
       cnt += __builtin_popcount(Pw[w]);
     }
     const int incl = wave_incl_scan(cnt);
-    const uint32_t base = wave_bits + (s.off0 & 31u) + static_cast<uint32_t>(incl - cnt);
+    const uint32_t base = stage_bits + wave_bits + (s.off0 & 31u) + static_cast<uint32_t>(incl - cnt);
     __builtin_amdgcn_wave_barrier();
     // Decode burst at raised wave priority (as in the matrix-core kernel).
     __builtin_amdgcn_s_setprio(1);
@@ -334,7 +337,8 @@ __global__ void __launch_bounds__(fast_threads(W, BF16)) bitcos_fast_kernel(cons
     // A word's 64-bit window of the sign block, aligned to its first sign.
     auto window = [&](int w) {
       const uint32_t b = base + static_cast<uint32_t>(pc[w]);
-      return __builtin_amdgcn_alignbit(scr32[(b >> 5) + 1], scr32[b >> 5], b);
+      LdsU32* wp = (LdsU32*)static_cast<size_t>((b >> 3) & ~3u);
+      return __builtin_amdgcn_alignbit(wp[1], wp[0], b);
     };
     if constexpr (FastCfg<W, BF16>::kPipelined) {
       Look<BF16> L = look(Pw[0], window(0), fl);

@@ -32,9 +32,10 @@
 //     summed exactly in int32 when the scale is per tensor.
 // Sign cursors: every row's entry comes from its offset entry (one per row);
 // in a step the four lanes of a row exchange their words' popcounts (one
-// byte per group) to place each word.  A row's signs for one step (at most
-// 512 bits, starting anywhere in a dword) are fetched as 20 dwords, staged
-// in the wave's LDS block and read as 64-bit windows.
+// byte per group, by permlane swaps between 16-lane rows) to place each
+// word.  A row's signs for one step (at most 512 bits, starting anywhere in
+// a dword) are fetched as 20 dwords, staged in the wave's LDS block and read
+// as 64-bit windows.
 // Pipeline: the presence words, group scales and sign dwords of step t+1 are
 // issued at the start of step t (the sign range of step t+1 follows from the
 // popcounts of step t).  Activations of step t+1 are issued during step t,
@@ -128,6 +129,7 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
 
   const int nr = lane & 15;
   const int g = lane >> 4;
+  const uint32_t gm1 = lane_mask((g & 1) != 0), gm2 = lane_mask((g & 2) != 0);
   const FastLane fl = fast_lane<BF16, CT>(lane);
   uint32_t* const stage = sstage + wv * (kMfmaRows * kSignStride);
   uint8_t* const xbuf = reinterpret_cast<uint8_t*>(xbufs) + wv * mfma_xbuf_bytes(BF16, STAGE);
@@ -203,23 +205,30 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
     uint32_t SB[RT];
     uint32_t pos[RT];
   };
+  // Every load splits its offset into a lane part (voffset) and a
+  // wave-uniform part (soffset: the unit's rows, the step, the group), so the
+  // addresses cost scalar instructions; a load with nothing to read gets
+  // soffset kOOB.
   auto issue = [&](const MStep& s, Slot& d) {
-    const int c = s.valid ? s.c : 0;
-    const int row0 = s.unit * kMfmaRows;
+    const uint32_t c = static_cast<uint32_t>(s.valid ? s.c : 0);
+    const uint32_t row0 = static_cast<uint32_t>(s.unit * kMfmaRows);
+    const uint32_t lp = (static_cast<uint32_t>(nr) * static_cast<uint32_t>(fupr) + g) * 4u;
+    const uint32_t ls = __umul24(static_cast<uint32_t>(nr), static_cast<uint32_t>(fG)) * 2u;
 #pragma unroll
     for (int r = 0; r < RT; ++r) {
-      const uint32_t row = static_cast<uint32_t>(row0 + kMfmaTile * r + nr);
-      const uint32_t pbase = (row * fupr + 16u * c + g) * 4u;
-      const uint32_t sbase = (row * fG + 4u * c) * 2u;
+      const uint32_t rowr = row0 + kMfmaTile * r;
+      const uint32_t sp = (rowr * static_cast<uint32_t>(fupr) + 16u * c) * 4u;
+      const uint32_t ss = (rowr * static_cast<uint32_t>(fG) + 4u * c) * 2u;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const bool ok = s.valid && 4 * c + q < fG;
-        d.P[r][q] = ld32(rb, ok ? pbase + 16u * q : kOOB);
-        d.SC[r][q] = ld16(rs, ok ? sbase + 2u * q : kOOB);
+        const bool ok = s.valid && static_cast<int>(4 * c) + q < fG;
+        d.P[r][q] = __builtin_amdgcn_raw_buffer_load_b32(rb, lp, __builtin_amdgcn_readfirstlane(ok ? sp + 16u * q : kOOB), 0);
+        d.SC[r][q] = __builtin_amdgcn_raw_buffer_load_b16(rs, ls, __builtin_amdgcn_readfirstlane(ok ? ss + 2u * q : kOOB), 0);
       }
       const uint32_t sdw = d.pos[r] >> 5;
-      d.SA[r] = ld128(rg, s.valid ? (sdw + 4u * g) * 4u : kOOB);
-      d.SB[r] = ld32(rg, s.valid ? (sdw + 16u + g) * 4u : kOOB);
+      const uint32_t sv = __builtin_amdgcn_readfirstlane(s.valid ? 0u : kOOB);
+      d.SA[r] = ld128_s(rg, (sdw + 4u * g) * 4u, sv);
+      d.SB[r] = __builtin_amdgcn_raw_buffer_load_b32(rg, (sdw + 16u + g) * 4u, sv, 0);
     }
   };
   // Activations of group q of a step: 32 of batch row nr at the lane's word
@@ -227,28 +236,32 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
   u32x4_t A[4][NA];
   float XA[4][4];
   auto issue_x = [&](const MStep& s, int q) {
-    const int gi = 4 * (s.valid ? s.c : 0) + q;
-    const bool ok = s.valid && gi < fG;
+    const uint32_t gi = static_cast<uint32_t>(4 * (s.valid ? s.c : 0) + q);
+    const bool ok = s.valid && static_cast<int>(gi) < fG;
+    const uint32_t ukk = static_cast<uint32_t>(fk);
     if constexpr (STAGE) {
-      // Coalesced: load jj covers batch rows XLR/4... of the group, each row's
-      // 128 activations as contiguous 16-byte pieces (lane l: row
+      // Coalesced: load jj covers batch rows (64 / XLR) jj .. of the group,
+      // each row's 128 activations as contiguous 16-byte pieces (lane l: row
       // (64 / XLR) jj + l / XLR, piece l % XLR).
+      const uint32_t lx = static_cast<uint32_t>(lane / XLR) * ukk * ELEM + 16u * static_cast<uint32_t>(lane % XLR);
 #pragma unroll
       for (int jj = 0; jj < NA; ++jj) {
-        const uint32_t row = static_cast<uint32_t>((64 / XLR) * jj + lane / XLR);
-        const uint32_t off = ok ? (row * fk + 128u * gi) * ELEM + 16u * static_cast<uint32_t>(lane % XLR) : kOOB;
-        A[q][jj] = ld128(rx, off);
+        const uint32_t so = (static_cast<uint32_t>((64 / XLR) * jj) * ukk + 128u * gi) * ELEM;
+        A[q][jj] = ld128_s(rx, lx, __builtin_amdgcn_readfirstlane(ok ? so : kOOB));
       }
     } else {
-      const uint32_t off = ok ? (static_cast<uint32_t>(nr * fk) + 128u * gi + 32u * g) * ELEM : kOOB;
+      const uint32_t lx = (static_cast<uint32_t>(nr) * ukk + 32u * g) * ELEM;
+      const uint32_t so = __builtin_amdgcn_readfirstlane(ok ? 128u * gi * ELEM : kOOB);
 #pragma unroll
-      for (int j = 0; j < NA; ++j) A[q][j] = ld128(rx, off + 16u * j);
+      for (int j = 0; j < NA; ++j) A[q][j] = ld128_s(rx, lx + 16u * j, so);
     }
     if constexpr (XS) {
+      const uint32_t la = __umul24(4u * g, static_cast<uint32_t>(fG)) * 4u;
 #pragma unroll
       for (int i = 0; i < 4; ++i)
         XA[q][i] = __builtin_bit_cast(
-            float, ld32(rxs, ok ? (static_cast<uint32_t>((4 * g + i) * fG) + gi) * 4u : kOOB));
+            float, __builtin_amdgcn_raw_buffer_load_b32(
+                       rxs, la, __builtin_amdgcn_readfirstlane(ok ? (static_cast<uint32_t>(i * fG) + gi) * 4u : kOOB), 0));
     }
   };
   auto advance = [&](const MStep& s) {
@@ -325,10 +338,10 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
       uint32_t v = 0;
 #pragma unroll
       for (int q = 0; q < 4; ++q) v |= static_cast<uint32_t>(__builtin_popcount(cur.P[r][q])) << (8 * q);
-      const uint32_t b = static_cast<uint32_t>(__shfl_xor(static_cast<int>(v), 16, kWave));
+      const uint32_t b = xor16(v);
       const uint32_t pair = v + b;
-      const uint32_t c2 = static_cast<uint32_t>(__shfl_xor(static_cast<int>(pair), 32, kWave));
-      const uint32_t excl = ((g & 1) ? b : 0u) + ((g & 2) ? c2 : 0u);
+      const uint32_t c2 = xor32(pair);
+      const uint32_t excl = (b & gm1) + (c2 & gm2);
       const uint32_t tot = pair + c2;  // bytes <= 128
       uint32_t cum = cur.pos[r] & 31u;
 #pragma unroll

@@ -1,5 +1,5 @@
 // Pieces shared by the kernels that multiply on the matrix cores: MFMA
-// operand vector types and 16-byte buffer loads.
+// operand vector types, 16-byte buffer loads and cross-lane helpers.
 #pragma once
 
 #include "bitcos_kernel.h"
@@ -16,6 +16,29 @@ __device__ __forceinline__ u32x4_t ld128(rsrc_t r, uint32_t off) {
 }
 __device__ __forceinline__ u32x4_t ld128_s(rsrc_t r, uint32_t voff, uint32_t soff) {
   return __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+
+// A per-lane all-ones / all-zeros mask the compiler cannot see through.
+// Conditions on cross-lane results are applied with these masks instead of
+// selects: a select may be turned into a branch around the DPP or permlane
+// move, which then runs with lanes switched off and reads them as zero.
+__device__ __forceinline__ uint32_t lane_mask(bool on) {
+  uint32_t m = on ? ~0u : 0u;
+  asm volatile("" : "+v"(m));
+  return m;
+}
+
+// The value of lane l ^ 16 and of lane l ^ 32: v_permlane16_swap exchanges
+// the 16-lane rows of the pairs (0,1) and (2,3), v_permlane32_swap the wave's
+// halves; with v in both operands the two results are v and the partner's
+// value, so the partner's is their sum minus v (exact in modular arithmetic).
+__device__ __forceinline__ uint32_t xor16(uint32_t v) {
+  const auto p = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  return p[0] + p[1] - v;
+}
+__device__ __forceinline__ uint32_t xor32(uint32_t v) {
+  const auto p = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return p[0] + p[1] - v;
 }
 
 }  // namespace bitcos_k
