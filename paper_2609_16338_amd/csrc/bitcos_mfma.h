@@ -24,8 +24,8 @@
 //   * A operand (activations, 16 batch rows x K): lane (m, g) holds batch row
 //     m's activations at the positions its B partner decodes; rows m >= M
 //     read zero through the buffer range check, so one kernel serves every M.
-//     Loaded directly, or (staged) in whole 16-byte pieces per batch row and
-//     handed to the lanes through a per-wave LDS transpose buffer.
+//     Loaded in whole 16-byte pieces per batch row and handed to the lanes
+//     through a per-wave LDS transpose buffer.
 //   * C (16 batch rows x 16 output rows): lane l holds batch rows
 //     4 (l / 16) + i of output row l % 16.  Every group's C is scaled into
 //     fp32 accumulators (fp16 group scale x activation scale, Sec. II-C), or
@@ -70,21 +70,19 @@ constexpr bool mfma_lookahead(bool bf16) {
   (void)bf16;
   return true;
 }
-// Activation loads.  Direct: lane (m, g) reads batch row m at its word (16
-// bytes per load, every load touching 16 rows x 2 cache lines).  Staged:
-// each load reads whole 16-byte pieces of a few batch rows in order (fully
-// used lines) and the wave's transpose buffer in LDS hands every lane its
-// MFMA operand; it adds an LDS round trip per group but touches a quarter of
-// the lines.  On 8 Qwen3-32B-like layers (us per step, bf16 / int8): direct
-// 595 / 721 at M = 4 and 840 / 781 at M = 16; staged 714 / 706 at M = 4 and
-// 719 / 714 at M = 16.
+// Activation loads: each load reads whole 16-byte pieces of a few batch
+// rows in order (fully used cache lines) and the wave's transpose buffer in
+// LDS hands every lane its MFMA operand.  Loading each lane's operand
+// directly (16 bytes of batch row m at the lane's word: every load touches
+// 16 rows x 2 cache lines) measured slower at every M (8 Qwen3-32B-like
+// layers, us per step, bf16 / int8: 597 / 576 against 573 / 576 at M = 4,
+// 843 / 670 against 651 / 611 at M = 16).
 constexpr int mfma_xrow(bool bf16) { return (bf16 ? 256 : 128) + 16; }  // one group's activations of a batch row, padded
-constexpr int mfma_xbuf_bytes(bool bf16, bool stage) { return stage ? 16 * mfma_xrow(bf16) : 16; }
-constexpr bool mfma_staged(int m, bool bf16) { return !bf16 || m > 8; }
+constexpr int mfma_xbuf_bytes(bool bf16) { return 16 * mfma_xrow(bf16); }
 // Sign-table copies (tables.h): 32 when the tables and the waves' sign
 // stages fit the LDS, else 16.
-constexpr int mfma_sign_copies(bool bf16, bool stage) {
-  return 65536 + 2048 * 32 + (mfma_threads(bf16, false) / 64) * (kMfmaRows * kSignStride * 4 + mfma_xbuf_bytes(bf16, stage)) <=
+constexpr int mfma_sign_copies(bool bf16) {
+  return 65536 + 2048 * 32 + (mfma_threads(bf16, false) / 64) * (kMfmaRows * kSignStride * 4 + mfma_xbuf_bytes(bf16)) <=
                  kLdsBytes
              ? 32
              : 16;
@@ -99,9 +97,9 @@ struct MStep {
   bool valid;
 };
 
-template <bool BF16, bool XS, bool TABLE, bool STAGE>
+template <bool BF16, bool XS, bool TABLE>
 __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(const KernelArgs a) {
-  constexpr int CT = mfma_sign_copies(BF16, STAGE);
+  constexpr int CT = mfma_sign_copies(BF16);
   constexpr int THREADS = mfma_threads(BF16, XS);
   constexpr int WPB = THREADS / kWave;
   constexpr int RT = kMfmaRT;
@@ -111,7 +109,7 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
 
   __shared__ FastTables<BF16, CT> tab;
   __shared__ uint32_t sstage[WPB * kMfmaRows * kSignStride];
-  __shared__ uint4 xbufs[WPB * mfma_xbuf_bytes(BF16, STAGE) / 16];
+  __shared__ uint4 xbufs[WPB * mfma_xbuf_bytes(BF16) / 16];
   static_assert(sizeof(tab) + sizeof(sstage) + sizeof(xbufs) <= kLdsBytes, "small-batch kernel LDS");
   build_fast_tables<BF16, CT>(tab, threadIdx.x, THREADS);
   __syncthreads();
@@ -132,7 +130,7 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
   const uint32_t gm1 = lane_mask((g & 1) != 0), gm2 = lane_mask((g & 2) != 0);
   const FastLane fl = fast_lane<BF16, CT>(lane);
   uint32_t* const stage = sstage + wv * (kMfmaRows * kSignStride);
-  uint8_t* const xbuf = reinterpret_cast<uint8_t*>(xbufs) + wv * mfma_xbuf_bytes(BF16, STAGE);
+  uint8_t* const xbuf = reinterpret_cast<uint8_t*>(xbufs) + wv * mfma_xbuf_bytes(BF16);
   constexpr int XROW = mfma_xrow(BF16);
   constexpr int XLR = BF16 ? 16 : 8;  // lanes per batch row in a coalesced load (16-byte pieces)
 
@@ -239,21 +237,14 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
     const uint32_t gi = static_cast<uint32_t>(4 * (s.valid ? s.c : 0) + q);
     const bool ok = s.valid && static_cast<int>(gi) < fG;
     const uint32_t ukk = static_cast<uint32_t>(fk);
-    if constexpr (STAGE) {
-      // Coalesced: load jj covers batch rows (64 / XLR) jj .. of the group,
-      // each row's 128 activations as contiguous 16-byte pieces (lane l: row
-      // (64 / XLR) jj + l / XLR, piece l % XLR).
-      const uint32_t lx = static_cast<uint32_t>(lane / XLR) * ukk * ELEM + 16u * static_cast<uint32_t>(lane % XLR);
+    // Load jj covers batch rows (64 / XLR) jj .. of the group, each row's 128
+    // activations as contiguous 16-byte pieces (lane l: row (64 / XLR) jj +
+    // l / XLR, piece l % XLR).
+    const uint32_t lx = static_cast<uint32_t>(lane / XLR) * ukk * ELEM + 16u * static_cast<uint32_t>(lane % XLR);
 #pragma unroll
-      for (int jj = 0; jj < NA; ++jj) {
-        const uint32_t so = (static_cast<uint32_t>((64 / XLR) * jj) * ukk + 128u * gi) * ELEM;
-        A[q][jj] = ld128_s(rx, lx, __builtin_amdgcn_readfirstlane(ok ? so : kOOB));
-      }
-    } else {
-      const uint32_t lx = (static_cast<uint32_t>(nr) * ukk + 32u * g) * ELEM;
-      const uint32_t so = __builtin_amdgcn_readfirstlane(ok ? 128u * gi * ELEM : kOOB);
-#pragma unroll
-      for (int j = 0; j < NA; ++j) A[q][j] = ld128_s(rx, lx + 16u * j, so);
+    for (int jj = 0; jj < NA; ++jj) {
+      const uint32_t so = (static_cast<uint32_t>((64 / XLR) * jj) * ukk + 128u * gi) * ELEM;
+      A[q][jj] = ld128_s(rx, lx, __builtin_amdgcn_readfirstlane(ok ? so : kOOB));
     }
     if constexpr (XS) {
       const uint32_t la = __umul24(4u * g, static_cast<uint32_t>(fG)) * 4u;
@@ -314,6 +305,47 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
 #pragma unroll
   for (int q = 0; q < 4; ++q) issue_x(fs, q);
 
+  // A step's word positions and staged signs are prepared at the end of the
+  // step before it (the prologue for the first), while that step's MFMAs
+  // drain, so a step starts with its window reads.
+  // Word positions: popcounts exchanged among the four lanes of each row.
+  uint32_t rel[RT][4];
+  uint32_t stot[RT];
+  auto place = [&](const Slot& sl) {
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+      uint32_t v = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v |= static_cast<uint32_t>(__builtin_popcount(sl.P[r][q])) << (8 * q);
+      const uint32_t b = xor16(v);
+      const uint32_t pair = v + b;
+      const uint32_t c2 = xor32(pair);
+      const uint32_t excl = (b & gm1) + (c2 & gm2);
+      const uint32_t tot = pair + c2;  // bytes <= 128
+      uint32_t cum = sl.pos[r] & 31u;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        rel[r][q] = cum + __builtin_amdgcn_ubfe(excl, 8 * q, 8);
+        cum += __builtin_amdgcn_ubfe(tot, 8 * q, 8);
+      }
+      stot[r] = cum - (sl.pos[r] & 31u);
+    }
+  };
+  // A step's sign dwords into the wave's LDS block (the previous step's
+  // window reads have all returned: their lookups fed its MFMAs).
+  auto stage_signs = [&](const Slot& sl) {
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+      uint32_t* row = stage + (kMfmaTile * r + nr) * kSignStride;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) row[4 * g + j] = sl.SA[r][j];
+      row[16 + g] = sl.SB[r];
+    }
+    __builtin_amdgcn_wave_barrier();
+  };
+  place(cur);
+  stage_signs(cur);
+
   for (;;) {
     const MStep cs = fs;
     if (!cs.valid) break;
@@ -330,28 +362,6 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
       ry = make_rsrc(D.y, D.y_bytes);
     }
 
-    // Word positions: popcounts exchanged among the four lanes of each row.
-    uint32_t rel[RT][4];
-    uint32_t stot[RT];
-#pragma unroll
-    for (int r = 0; r < RT; ++r) {
-      uint32_t v = 0;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) v |= static_cast<uint32_t>(__builtin_popcount(cur.P[r][q])) << (8 * q);
-      const uint32_t b = xor16(v);
-      const uint32_t pair = v + b;
-      const uint32_t c2 = xor32(pair);
-      const uint32_t excl = (b & gm1) + (c2 & gm2);
-      const uint32_t tot = pair + c2;  // bytes <= 128
-      uint32_t cum = cur.pos[r] & 31u;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        rel[r][q] = cum + __builtin_amdgcn_ubfe(excl, 8 * q, 8);
-        cum += __builtin_amdgcn_ubfe(tot, 8 * q, 8);
-      }
-      stot[r] = cum - (cur.pos[r] & 31u);
-    }
-
     // Fetch step t+1.  offn holds the offsets of the unit after step t's:
     // step t+1's own when it starts a unit.  They are reloaded every step,
     // unconditionally: loads in a branch into a loop-carried register make
@@ -362,16 +372,6 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
     for (int r = 0; r < RT; ++r) nxt.pos[r] = fs.c == 0 ? offn[r] : cur.pos[r] + stot[r];
     next_unit_offsets(fs.unit, offn);
     issue(fs, nxt);
-
-    // This step's sign dwords into the wave's LDS block.
-#pragma unroll
-    for (int r = 0; r < RT; ++r) {
-      uint32_t* row = stage + (kMfmaTile * r + nr) * kSignStride;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) row[4 * g + j] = cur.SA[r][j];
-      row[16 + g] = cur.SB[r];
-    }
-    __builtin_amdgcn_wave_barrier();
 
     // The groups at raised wave priority (as in the batch-1 kernels): int8
     // 9 % faster at M = 4 on the Qwen3-32B-like layers, bf16 1.5 %.
@@ -440,19 +440,14 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
 #pragma unroll
         for (int r = 0; r < RT; ++r) lk[(q + 1) & 1][r] = lookup1(q + 1, r);
       }
-      // The group's activations in MFMA order: lane (nr, g) takes batch row
-      // nr at its word's pieces (staged: through the wave's transpose buffer).
+      // The group's activations in MFMA order, through the wave's transpose
+      // buffer: lane (nr, g) takes batch row nr at its word's pieces.
       u32x4_t Aq[NA];
-      if constexpr (STAGE) {
 #pragma unroll
-        for (int jj = 0; jj < NA; ++jj)
-          *reinterpret_cast<u32x4_t*>(xbuf + ((64 / XLR) * jj + lane / XLR) * XROW + 16 * (lane % XLR)) = A[q][jj];
+      for (int jj = 0; jj < NA; ++jj)
+        *reinterpret_cast<u32x4_t*>(xbuf + ((64 / XLR) * jj + lane / XLR) * XROW + 16 * (lane % XLR)) = A[q][jj];
 #pragma unroll
-        for (int j = 0; j < NA; ++j) Aq[j] = *reinterpret_cast<const u32x4_t*>(xbuf + nr * XROW + 16 * (NA * g + j));
-      } else {
-#pragma unroll
-        for (int j = 0; j < NA; ++j) Aq[j] = A[q][j];
-      }
+      for (int j = 0; j < NA; ++j) Aq[j] = *reinterpret_cast<const u32x4_t*>(xbuf + nr * XROW + 16 * (NA * g + j));
       CV c[RT];
 #pragma unroll
       for (int r = 0; r < RT; ++r) c[r] = CV{0, 0, 0, 0};
@@ -506,6 +501,9 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
         }
       }
     }
+    // The next step's positions and signs (its loads were issued a step ago).
+    place(nxt);
+    stage_signs(nxt);
     cur = nxt;
   }
 }
@@ -513,14 +511,13 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
 using MfmaFn = void (*)(const KernelArgs);
 
 template <bool BF16, bool XS>
-MfmaFn pick_mfma_t(bool table, bool stage) {
-  if (stage) return table ? bitcos_mfma_kernel<BF16, XS, true, true> : bitcos_mfma_kernel<BF16, XS, false, true>;
-  return table ? bitcos_mfma_kernel<BF16, XS, true, false> : bitcos_mfma_kernel<BF16, XS, false, false>;
+MfmaFn pick_mfma_t(bool table) {
+  return table ? bitcos_mfma_kernel<BF16, XS, true> : bitcos_mfma_kernel<BF16, XS, false>;
 }
 
-inline MfmaFn pick_mfma(bool bf16, bool xs, bool table, bool stage) {
-  if (bf16) return xs ? pick_mfma_t<true, true>(table, stage) : pick_mfma_t<true, false>(table, stage);
-  return xs ? pick_mfma_t<false, true>(table, stage) : pick_mfma_t<false, false>(table, stage);
+inline MfmaFn pick_mfma(bool bf16, bool xs, bool table) {
+  if (bf16) return xs ? pick_mfma_t<true, true>(table) : pick_mfma_t<true, false>(table);
+  return xs ? pick_mfma_t<false, true>(table) : pick_mfma_t<false, false>(table);
 }
 
 }  // namespace bitcos_k

@@ -18,8 +18,7 @@ int launch_bitcos_mfma(const BatchHeader& h, const GemvDesc* table_dev, const Ge
   if (h.m == 1 && !h.small_batch) return BITCOS_E_UNSUPPORTED;
   if (h.total_units < 1 || h.total_units >= (int64_t(1) << 31)) return BITCOS_E_UNSUPPORTED;
   const bool bf16 = h.x_dtype == BITCOS_X_BF16;
-  bitcos_k::MfmaFn fn =
-      bitcos_k::pick_mfma(bf16, h.any_xscale != 0, table_dev != nullptr, bitcos_k::mfma_staged(h.m, bf16));
+  bitcos_k::MfmaFn fn = bitcos_k::pick_mfma(bf16, h.any_xscale != 0, table_dev != nullptr);
   bitcos_k::KernelArgs a;
   a.table = table_dev;
   a.total_units = h.total_units;
