@@ -118,8 +118,9 @@ def emit(obj, args):
 KERNEL_SOURCES = ["bitcos_diag.h", "bitcos_fast.h", "bitcos_kernel.h", "bitcos_mfma.h", "mfma_common.h", "tables.h",
                   "device_common.h", "batch.h", "batch.hip", "gemv_bitcos.hip", "launch_common.h", "plan.h"]
 TRAFFIC_FILES = {
-    "qwen3_32b_layers": os.path.join(ROOT, "profiles", "bitcos_fast_bf16_qwen3_32b_k5120_traffic.txt"),
-    "bitnet2b_layers": os.path.join(ROOT, "profiles", "bitcos_diag_bf16_bitnet2b_k2560_traffic.txt"),
+    "qwen3_32b_layers": [os.path.join(ROOT, "profiles", f) for f in (
+        "bitcos_fast_bf16_qwen3_32b_k5120_traffic.txt", "bitcos_mfma_bf16_qwen3_32b_m16_traffic.txt")],
+    "bitnet2b_layers": [os.path.join(ROOT, "profiles", "bitcos_diag_bf16_bitnet2b_k2560_traffic.txt")],
 }
 COPY_MIB = 256
 
@@ -133,27 +134,38 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def stored_traffic(workload, kernel):
-    """HBM bytes per launch of the dominant kernel from the FETCH_SIZE / WRITE_SIZE
-    passes (scaled by the copy calibration), or None if the kernel changed since
-    or the stored launch is another kernel or tile than `kernel` (say
-    "bitcos_fast_kernel<5, 32,": a small-batch run of the same set launches
-    a different kernel)."""
-    path = TRAFFIC_FILES.get(workload)
-    try:
-        with open(path) as f:
-            kv = dict(line.split(":", 1) for line in f if ":" in line and not line.startswith("#"))
-    except (OSError, TypeError):
-        return None
-    kv = {k.strip(): v.strip() for k, v in kv.items()}
-    if kv.get("kernel_source_hash") != kernel_source_hash():
-        return None
-    if kernel not in kv.get("kernel", ""):
-        return None
-    try:
-        return int(float(kv["traffic_bytes_per_launch"]))
-    except (KeyError, ValueError):
-        return None
+def stored_traffic(workload, launch):
+    """HBM bytes per launch of the dominant launch from the FETCH_SIZE / WRITE_SIZE
+    passes (scaled by the copy calibration): from the stored measurement of
+    the same launch (`launch`: its label, say "bitcos_fast_kernel<5,32,bf16,
+    table>: 448 GEMVs in one launch"), or None if there is none or the kernel
+    sources changed since it was taken."""
+    for path in TRAFFIC_FILES.get(workload, []):
+        try:
+            with open(path) as f:
+                kv = dict(line.split(":", 1) for line in f if ":" in line and not line.startswith("#"))
+        except OSError:
+            continue
+        kv = {k.strip(): v.strip() for k, v in kv.items()}
+        if kv.get("launch") != launch or kv.get("kernel_source_hash") != kernel_source_hash():
+            continue
+        try:
+            return int(float(kv["traffic_bytes_per_launch"]))
+        except (KeyError, ValueError):
+            return None
+    return None
+
+
+def launch_label(top, m):
+    """Kernel, tile and GEMV count of a batched launch (bf16 activations)."""
+    from paper_2609_16338_amd import _native as N
+    from paper_2609_16338_amd import api
+
+    kinds = {api.describe(e[3], m, N.X_BF16).kernel for e in top.entries}
+    kname = {N.KERNEL_MATRIX: "bitcos_diag_kernel", N.KERNEL_STREAMING: "bitcos_fast_kernel",
+             N.KERNEL_GENERAL: "bitcos_gemv_kernel", N.KERNEL_SMALL_BATCH: "bitcos_mfma_kernel",
+             }.get(kinds.pop(), "?") if len(kinds) == 1 else "mixed"
+    return f"{kname}<{top.tile[0]},{top.tile[1]},bf16,table>: {len(top.entries)} GEMVs in one launch"
 
 
 # ---------------------------------------------------------------------------
@@ -659,10 +671,7 @@ def dominant_roofline(r, args, name):
     top_weights = sum(e[3].n * e[3].k for e in top.entries)
     launch_gamma = 32 * CU_COUNT * CLOCK_HZ * per_launch_us * 1e-6 / top_weights
     hbm_term = 32 * alg_bytes / top_weights / (HBM_PEAK_GBS * 1e9 / (CU_COUNT * CLOCK_HZ))
-    kinds = {api.describe(e[3], m, N.X_BF16).kernel for e in top.entries}
-    kname = {N.KERNEL_MATRIX: "bitcos_diag_kernel", N.KERNEL_STREAMING: "bitcos_fast_kernel",
-             N.KERNEL_GENERAL: "bitcos_gemv_kernel", N.KERNEL_SMALL_BATCH: "bitcos_mfma_kernel",
-             }.get(kinds.pop(), "?") if len(kinds) == 1 else "mixed"
+    label = launch_label(top, m)
     return {
         # The roofline the metric is read against (weight bytes per second vs
         # HBM peak); what limits the kernel today is the larger two_term term,
@@ -673,8 +682,8 @@ def dominant_roofline(r, args, name):
         "peak": HBM_PEAK_GBS,
         "unit": "GB/s",
         "frac": round(achieved / HBM_PEAK_GBS, 4),
-        "traffic": stored_traffic(name, f"{kname}<{top.tile[0]}, {top.tile[1]},"),
-        "kernel": f"{kname}<{top.tile[0]},{top.tile[1]},bf16,table>: {len(top.entries)} GEMVs in one launch",
+        "traffic": stored_traffic(name, label),
+        "kernel": label,
         "per_launch_us": round(per_launch_us, 3),
         "bytes_per_launch": int(alg_bytes),
         "weights_per_launch": int(top_weights),
@@ -760,7 +769,7 @@ def profile_pass(args):
         dst.copy_(src)
     torch.cuda.synchronize()
     alg = sum(e[3].payload_bits / 8 + args.batch * (e[3].k * 2 + e[3].n * 4) for e in top.entries)
-    print(f"[profile-pass] {args.workload} dominant launch: {len(top.entries)} GEMVs, tile {top.tile}, "
+    print(f"[profile-pass] {args.workload} dominant launch: {launch_label(top, args.batch)}, "
           f"algorithmic bytes {int(alg)}; copy {COPY_MIB} MiB; kernel_source_hash {kernel_source_hash()}",
           flush=True)
 

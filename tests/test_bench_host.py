@@ -157,15 +157,19 @@ def test_column_blocks_split_only_long_rows():
         assert [k0 for k0, _ in blocks] == list(range(0, k, blocks[0][1]))
 
 
-def test_stored_traffic_only_for_the_measured_kernel_and_tile():
-    """A stored FETCH/WRITE measurement belongs to one kernel and tile: a run
-    of the same layer set on another kernel (the small-batch one at M > 1)
-    must report traffic as unmeasured, not borrow the batch-1 figure."""
-    with open(bench.TRAFFIC_FILES["qwen3_32b_layers"]) as f:
-        kernel = next(line.split(":", 1)[1].strip() for line in f if line.startswith("kernel:"))
-    measured = kernel.split("::")[-1].split("<")[0]
-    tile = kernel.split("<")[1].split(",")[:2]
-    other = "bitcos_mfma_kernel" if measured != "bitcos_mfma_kernel" else "bitcos_fast_kernel"
-    assert bench.stored_traffic("qwen3_32b_layers", f"{other}<{tile[0]},{tile[1]},") is None
-    assert bench.stored_traffic("qwen3_32b_layers", f"{measured}<{int(tile[0]) + 1}, {tile[1].strip()},") is None
-    assert bench.stored_traffic("no_such_set", f"{measured}<") is None
+def test_stored_traffic_only_for_the_measured_launch():
+    """A stored FETCH/WRITE measurement belongs to one launch (kernel, tile and
+    GEMV count): a run of the same layer set on another kernel (the
+    small-batch one at M > 1) or over other GEMVs must report traffic as
+    unmeasured, not borrow another launch's figure."""
+    path = bench.TRAFFIC_FILES["qwen3_32b_layers"][0]
+    with open(path) as f:
+        kv = dict(line.split(":", 1) for line in f if ":" in line and not line.startswith("#"))
+    launch = kv["launch"].strip()
+    kernel, rest = launch.split("<", 1)
+    other = "bitcos_mfma_kernel" if kernel != "bitcos_mfma_kernel" else "bitcos_fast_kernel"
+    assert bench.stored_traffic("qwen3_32b_layers", f"{other}<{rest}") is None
+    assert bench.stored_traffic("qwen3_32b_layers", launch.replace(" GEMVs", "0 GEMVs")) is None
+    assert bench.stored_traffic("no_such_set", launch) is None
+    if kv["kernel_source_hash"].strip() == bench.kernel_source_hash():
+        assert bench.stored_traffic("qwen3_32b_layers", launch) == int(float(kv["traffic_bytes_per_launch"]))
