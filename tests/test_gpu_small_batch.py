@@ -102,6 +102,22 @@ def test_small_batch_activation_scales(m, group):
     _check(y, w, sc, group, q, "int8", raw=True)
 
 
+@pytest.mark.parametrize("m", [1, 4, 16])
+@pytest.mark.parametrize("group", [0, 128])
+def test_small_batch_bf16_activation_scales(m, group):
+    """bf16 activations with per-group activation scales, y = sum_g S a A:
+    the small-batch kernel's bf16 activation-scale variant (at m = 1 through
+    a row too long for the batch-1 kernels)."""
+    n, k = (37, 20480) if m == 1 else (70, 2560)
+    w, sc = inputs(n, k, 0.42, group, 535 + m)
+    xb = _acts("bf16", m, k, 5)
+    a = wl.rng_for(536, m, k).uniform(0.5, 2.0, size=(m, k // 128)).astype(np.float32)
+    y, L = run(N.FMT_BITCOS, w, sc, group, xb, "bf16", xscale=a)
+    assert api.describe(L, m, N.X_BF16).kernel == N.KERNEL_SMALL_BATCH
+    ref = O.dense_gemv(w, sc, group, xb, a, x_is_bf16_bits=True)
+    check_bf16(y, ref, bf16_bound(w, sc, group, xb) * float(a.max()))
+
+
 @pytest.mark.parametrize("n,k", [(1, 128), (31, 128), (33, 640), (17, 384), (64, 12288), (5, 25600)])
 @pytest.mark.parametrize("kind", ["int8", "bf16"])
 def test_small_batch_ragged_shapes(n, k, kind):
