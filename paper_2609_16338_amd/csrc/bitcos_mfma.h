@@ -149,7 +149,10 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
     fupr = D.upr;
     rb = make_rsrc(D.sec0, D.sec0_bytes);
     rg = make_rsrc(D.signs, D.signs_bytes);
-    rs = make_rsrc(D.scales, (D.mode & kModeGrouped) ? D.scales_bytes : 0u);
+    // Scales are read three dwords at a time; a dword past the section reads
+    // zero, so the range is rounded up to whole dwords (at most two padding
+    // bytes of the blob, whose size is a multiple of 256).
+    rs = make_rsrc(D.scales, (D.mode & kModeGrouped) ? (D.scales_bytes + 3u) & ~3u : 0u);
     rx = make_rsrc(D.x, D.x_bytes);
     const bool xs = XS && (D.mode & kModeXscale);
     rxs = make_rsrc(xs ? D.xscale : nullptr, xs ? D.x_bytes / (32u * ELEM) : 0u);
@@ -198,7 +201,8 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
   // lane's row in each tile, and the row's sign position at the step start.
   struct Slot {
     uint32_t P[RT][4];
-    uint32_t SC[RT][4];
+    uint32_t SC[RT][3];  // the dwords holding the row's four fp16 group scales of the step
+    uint32_t SSH[RT];    // bit offset of the first scale in SC
     u32x4_t SA[RT];
     uint32_t SB[RT];
     uint32_t pos[RT];
@@ -221,8 +225,17 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
       for (int q = 0; q < 4; ++q) {
         const bool ok = s.valid && static_cast<int>(4 * c) + q < fG;
         d.P[r][q] = __builtin_amdgcn_raw_buffer_load_b32(rb, lp, __builtin_amdgcn_readfirstlane(ok ? sp + 16u * q : kOOB), 0);
-        d.SC[r][q] = __builtin_amdgcn_raw_buffer_load_b16(rs, ls, __builtin_amdgcn_readfirstlane(ok ? ss + 2u * q : kOOB), 0);
       }
+      // The step's four scales of the row (8 bytes at a 2-byte aligned
+      // offset) in one load of the three dwords that hold them.  Groups past
+      // the row's last (last step of a unit) read scales of the next row or
+      // zero; their products are zero.
+      const uint32_t sa = ls + ss;
+      const auto v3 = __builtin_amdgcn_raw_buffer_load_b96(rs, sa & ~3u, __builtin_amdgcn_readfirstlane(s.valid ? 0u : kOOB), 0);
+      d.SC[r][0] = v3[0];
+      d.SC[r][1] = v3[1];
+      d.SC[r][2] = v3[2];
+      d.SSH[r] = (sa & 2u) << 3;
       const uint32_t sdw = d.pos[r] >> 5;
       const uint32_t sv = __builtin_amdgcn_readfirstlane(s.valid ? 0u : kOOB);
       d.SA[r] = ld128_s(rg, (sdw + 4u * g) * 4u, sv);
@@ -384,7 +397,8 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
 #pragma unroll
       for (int r = 0; r < RT; ++r) {
         if (scaled) {
-          const float sc = (grouped ? half_bits_to_float(static_cast<uint16_t>(cur.SC[r][q])) : tscale) *
+          const uint32_t pair = __builtin_amdgcn_alignbit(cur.SC[r][q / 2 + 1], cur.SC[r][q / 2], cur.SSH[r]);
+          const float sc = (grouped ? half_bits_to_float(static_cast<uint16_t>(q & 1 ? pair >> 16 : pair)) : tscale) *
                            (BF16 ? 2.0f : 1.0f);
 #pragma unroll
           for (int i = 0; i < 4; ++i)
