@@ -136,7 +136,7 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
 
   // ---- fetch side: the GEMV whose step is being fetched; fbeg / fend: its
   // first step in the launch and one past its last, fC: steps per unit.
-  int fdi = 0, fbeg = 0, fend = 0, fC = 1, fG = 1, fk = 0, fupr = 0;
+  int fdi = 0, fbeg = 0, fend = 0, fC = 1, fG = 1, fk = 0, fupr = 0, fM = 0;
   rsrc_t rb = make_rsrc(nullptr, 0), rg = rb, rs = rb, rx = rb, rxs = rb;
   auto fetch_enter = [&](int d) {
     fdi = __builtin_amdgcn_readfirstlane(d);
@@ -146,6 +146,7 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
     fG = D.ngroups;
     fC = (fG + 3) >> 2;
     fk = D.upr * 32;
+    fM = static_cast<int>(D.x_bytes / (static_cast<uint32_t>(fk) * ELEM));  // activation rows
     fupr = D.upr;
     rb = make_rsrc(D.sec0, D.sec0_bytes);
     rg = make_rsrc(D.signs, D.signs_bytes);
@@ -254,10 +255,12 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
     // activations as contiguous 16-byte pieces (lane l: row (64 / XLR) jj +
     // l / XLR, piece l % XLR).
     const uint32_t lx = static_cast<uint32_t>(lane / XLR) * ukk * ELEM + 16u * static_cast<uint32_t>(lane % XLR);
+    // Loads whose batch rows are all past M are skipped: those rows' MFMA
+    // results are never stored, so stale registers there are harmless.
 #pragma unroll
     for (int jj = 0; jj < NA; ++jj) {
       const uint32_t so = (static_cast<uint32_t>((64 / XLR) * jj) * ukk + 128u * gi) * ELEM;
-      A[q][jj] = ld128_s(rx, lx, __builtin_amdgcn_readfirstlane(ok ? so : kOOB));
+      if (jj == 0 || (64 / XLR) * jj < fM) A[q][jj] = ld128_s(rx, lx, __builtin_amdgcn_readfirstlane(ok ? so : kOOB));
     }
     if constexpr (XS) {
       const uint32_t la = __umul24(4u * g, static_cast<uint32_t>(fG)) * 4u;
