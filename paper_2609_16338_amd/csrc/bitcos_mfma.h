@@ -215,18 +215,20 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
   auto issue = [&](const MStep& s, Slot& d) {
     const uint32_t c = static_cast<uint32_t>(s.valid ? s.c : 0);
     const uint32_t row0 = static_cast<uint32_t>(s.unit * kMfmaRows);
-    const uint32_t lp = (static_cast<uint32_t>(nr) * static_cast<uint32_t>(fupr) + g) * 4u;
+    // Presence: lane (nr, g) reads group g of the step (its four words, 16
+    // bytes); place() transposes the four lanes' groups so that each lane
+    // holds its word g of every group.
+    const uint32_t lp = (static_cast<uint32_t>(nr) * static_cast<uint32_t>(fupr) + 4u * g) * 4u;
+    const bool okg = s.valid && static_cast<int>(4 * c + g) < fG;
     const uint32_t ls = __umul24(static_cast<uint32_t>(nr), static_cast<uint32_t>(fG)) * 2u;
 #pragma unroll
     for (int r = 0; r < RT; ++r) {
       const uint32_t rowr = row0 + kMfmaTile * r;
       const uint32_t sp = (rowr * static_cast<uint32_t>(fupr) + 16u * c) * 4u;
       const uint32_t ss = (rowr * static_cast<uint32_t>(fG) + 4u * c) * 2u;
+      const u32x4_t pv = ld128_s(rb, okg ? lp : kOOB, __builtin_amdgcn_readfirstlane(s.valid ? sp : kOOB));
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const bool ok = s.valid && static_cast<int>(4 * c) + q < fG;
-        d.P[r][q] = __builtin_amdgcn_raw_buffer_load_b32(rb, lp, __builtin_amdgcn_readfirstlane(ok ? sp + 16u * q : kOOB), 0);
-      }
+      for (int q = 0; q < 4; ++q) d.P[r][q] = pv[q];
       // The step's four scales of the row (8 bytes at a 2-byte aligned
       // offset) in one load of the three dwords that hold them.  Groups past
       // the row's last (last step of a unit) read scales of the next row or
@@ -327,9 +329,10 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
   // Word positions: popcounts exchanged among the four lanes of each row.
   uint32_t rel[RT][4];
   uint32_t stot[RT];
-  auto place = [&](const Slot& sl) {
+  auto place = [&](Slot& sl) {
 #pragma unroll
     for (int r = 0; r < RT; ++r) {
+      transpose_lanes16(sl.P[r]);
       uint32_t v = 0;
 #pragma unroll
       for (int q = 0; q < 4; ++q) v |= static_cast<uint32_t>(__builtin_popcount(sl.P[r][q])) << (8 * q);

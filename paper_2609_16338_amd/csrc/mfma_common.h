@@ -41,4 +41,25 @@ __device__ __forceinline__ uint32_t xor32(uint32_t v) {
   return p[0] + p[1] - v;
 }
 
+// 4 x 4 transpose across the lanes l, l + 16, l + 32, l + 48: lane l + 16 a
+// ends with v[b] = what lane l + 16 b held in v[a].  Two butterfly levels:
+// v_permlane16_swap exchanges the odd 16-lane rows of its first operand with
+// the even rows of its second (rows a and a ^ 1, components b and b ^ 1),
+// v_permlane32_swap the upper half of its first operand with the lower half
+// of its second (rows a and a ^ 2, components b and b ^ 2).
+__device__ __forceinline__ void transpose_lanes16(uint32_t (&v)[4]) {
+  const auto s01 = __builtin_amdgcn_permlane16_swap(v[0], v[1], false, false);
+  const auto s23 = __builtin_amdgcn_permlane16_swap(v[2], v[3], false, false);
+  v[0] = s01[0];
+  v[1] = s01[1];
+  v[2] = s23[0];
+  v[3] = s23[1];
+  const auto s02 = __builtin_amdgcn_permlane32_swap(v[0], v[2], false, false);
+  const auto s13 = __builtin_amdgcn_permlane32_swap(v[1], v[3], false, false);
+  v[0] = s02[0];
+  v[2] = s02[1];
+  v[1] = s13[0];
+  v[3] = s13[1];
+}
+
 }  // namespace bitcos_k
