@@ -40,19 +40,6 @@
 
 namespace bitcos_k {
 
-template <class T>
-__device__ __forceinline__ T bits_as(uint32_t b) {
-  return __builtin_bit_cast(T, b);
-}
-template <class T>
-__device__ __forceinline__ uint32_t as_bits(T v) {
-  return __builtin_bit_cast(uint32_t, v);
-}
-template <int CTRL, class T>
-__device__ __forceinline__ T qperm(T v) {
-  return bits_as<T>(__builtin_amdgcn_update_dpp(0, as_bits(v), CTRL, 0xF, 0xF, false));
-}
-
 // Row sums of the diagonal elements.  Lane 16 (i/4) + i holds element i in
 // accumulator register i % 4, so in every quad on the diagonal (lanes 20a ..
 // 20a + 3) lane 20a + t holds register t.  Returns the row's total in the lane

@@ -248,7 +248,10 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
   // Activations of group q of a step: 32 of batch row nr at the lane's word
   // (and with XS, the activation scales of batch rows 4 g + i).
   u32x4_t A[4][NA];
-  float XA[4][4];
+  // Activation scales of the step (XS): lane (nr, g) holds batch row
+  // 4 g + nr % 4 at the step's four groups; a lane takes batch row 4 g + i's
+  // from lane i of its quad.
+  u32x4_t XV = {0u, 0u, 0u, 0u};
   auto issue_x = [&](const MStep& s, int q) {
     const uint32_t gi = static_cast<uint32_t>(4 * (s.valid ? s.c : 0) + q);
     const bool ok = s.valid && static_cast<int>(gi) < fG;
@@ -265,12 +268,10 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
       if (jj == 0 || (64 / XLR) * jj < fM) A[q][jj] = ld128_s(rx, lx, __builtin_amdgcn_readfirstlane(ok ? so : kOOB));
     }
     if constexpr (XS) {
-      const uint32_t la = __umul24(4u * g, static_cast<uint32_t>(fG)) * 4u;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        XA[q][i] = __builtin_bit_cast(
-            float, __builtin_amdgcn_raw_buffer_load_b32(
-                       rxs, la, __builtin_amdgcn_readfirstlane(ok ? (static_cast<uint32_t>(i * fG) + gi) * 4u : kOOB), 0));
+      if (q == 3) {  // after the step's last group: all four groups' scales in one load
+        const uint32_t la = static_cast<uint32_t>(4 * g + (nr & 3)) * static_cast<uint32_t>(fG) * 4u;
+        XV = ld128_s(rxs, la, __builtin_amdgcn_readfirstlane(s.valid ? 16u * static_cast<uint32_t>(s.c) : kOOB));
+      }
     }
   };
   auto advance = [&](const MStep& s) {
@@ -398,8 +399,15 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
     // Groups: the MFMAs of group q, then the epilogue of group q - 1 (whose
     // MFMAs have had a group's worth of work to finish).
     CV cg[2][RT];
-    float xa_prev[4];
-    auto epilogue = [&](int q, const CV (&c)[RT], const float (&xa)[4]) {
+    const u32x4_t xv = XV;  // this step's activation scales (the next step's load reuses XV)
+    auto epilogue = [&](int q, const CV (&c)[RT]) {
+      float xa[4] = {1.0f, 1.0f, 1.0f, 1.0f};
+      if (XS && dxs) {
+        xa[0] = qperm<0x00>(bits_as<float>(xv[q]));
+        xa[1] = qperm<0x55>(bits_as<float>(xv[q]));
+        xa[2] = qperm<0xAA>(bits_as<float>(xv[q]));
+        xa[3] = qperm<0xFF>(bits_as<float>(xv[q]));
+      }
 #pragma unroll
       for (int r = 0; r < RT; ++r) {
         if (scaled) {
@@ -487,15 +495,10 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
 #pragma unroll
       for (int r = 0; r < RT; ++r) cg[q & 1][r] = c[r];
       // This group's activations are consumed: fetch step t+1's.
-      float xa_q[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) xa_q[i] = XS ? XA[q][i] : 1.0f;
       issue_x(fs, q);
-      if (q > 0) epilogue(q - 1, cg[(q - 1) & 1], xa_prev);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) xa_prev[i] = xa_q[i];
+      if (q > 0) epilogue(q - 1, cg[(q - 1) & 1]);
     }
-    epilogue(3, cg[1], xa_prev);
+    epilogue(3, cg[1]);
     __builtin_amdgcn_s_setprio(0);
     __builtin_amdgcn_wave_barrier();
 

@@ -18,6 +18,20 @@ __device__ __forceinline__ u32x4_t ld128_s(rsrc_t r, uint32_t voff, uint32_t sof
   return __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
 }
 
+template <class T>
+__device__ __forceinline__ T bits_as(uint32_t b) {
+  return __builtin_bit_cast(T, b);
+}
+template <class T>
+__device__ __forceinline__ uint32_t as_bits(T v) {
+  return __builtin_bit_cast(uint32_t, v);
+}
+// A DPP quad permutation of v (CTRL: the quad_perm field).
+template <int CTRL, class T>
+__device__ __forceinline__ T qperm(T v) {
+  return bits_as<T>(__builtin_amdgcn_update_dpp(0, as_bits(v), CTRL, 0xF, 0xF, false));
+}
+
 // A per-lane all-ones / all-zeros mask the compiler cannot see through.
 // Conditions on cross-lane results are applied with these masks instead of
 // selects: a select may be turned into a branch around the DPP or permlane

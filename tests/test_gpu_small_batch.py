@@ -91,8 +91,11 @@ def test_small_batch_per_tensor_int8_bit_exact(m):
 
 @pytest.mark.parametrize("m", [3, 16])
 @pytest.mark.parametrize("group", [0, 128])
-def test_small_batch_activation_scales(m, group):
-    n, k = 70, 2560
+@pytest.mark.parametrize("k", [2560, 640, 1152])
+def test_small_batch_activation_scales(m, group, k):
+    # k = 640 and 1152: a group count that is not a multiple of four, so the
+    # last step of a unit has groups past the row's end
+    n = 70
     w, sc = inputs(n, k, 0.42, group, 530 + m)
     xb = _acts("bf16", m, k, 4)
     q, a = O.quantize_activations(xb)
