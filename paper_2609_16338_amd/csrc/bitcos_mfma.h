@@ -23,9 +23,10 @@
 //     v_mfma_f32_16x16x32_bf16 (the 0.5 is undone exactly at the end).
 //   * A operand (activations, 16 batch rows x K): lane (m, g) holds batch row
 //     m's activations at the positions its B partner decodes; rows m >= M
-//     read zero through the buffer range check, so one kernel serves every M.
-//     Loaded in whole 16-byte pieces per batch row and handed to the lanes
-//     through a per-wave LDS transpose buffer.
+//     read zero through the buffer range check, so one kernel serves every M
+//     (loads whose rows are all past M are skipped).  Loaded in whole 16-byte
+//     pieces per batch row and handed to the lanes through a per-wave LDS
+//     transpose buffer.
 //   * C (16 batch rows x 16 output rows): lane l holds batch rows
 //     4 (l / 16) + i of output row l % 16.  Every group's C is scaled into
 //     fp32 accumulators (fp16 group scale x activation scale, Sec. II-C), or
@@ -36,6 +37,11 @@
 // word.  A row's signs for one step (at most 512 bits, starting anywhere in
 // a dword) are fetched as 20 dwords, staged in the wave's LDS block and read
 // as 64-bit windows.
+// Loads: the kernel is bound by the count of its loads more than by their
+// bytes, so each row's data of a step comes in as few as possible: its
+// presence words in one 16-byte load per lane (group g, then transposed
+// across the row's four lanes), its four group scales in one 12-byte load,
+// the activation scales in one 16-byte load per lane shared across quads.
 // Pipeline: the presence words, group scales and sign dwords of step t+1 are
 // issued at the start of step t (the sign range of step t+1 follows from the
 // popcounts of step t).  Activations of step t+1 are issued during step t,
