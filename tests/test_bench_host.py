@@ -1,6 +1,7 @@
 """CPU tests of bench.py's host logic (no GPU: torch's graph calls are stubbed)."""
 
 import contextlib
+import os
 import gc
 import weakref
 
@@ -173,3 +174,20 @@ def test_stored_traffic_only_for_the_measured_launch():
     assert bench.stored_traffic("no_such_set", launch) is None
     if kv["kernel_source_hash"].strip() == bench.kernel_source_hash():
         assert bench.stored_traffic("qwen3_32b_layers", launch) == int(float(kv["traffic_bytes_per_launch"]))
+
+
+def test_kernel_source_hash_ignores_comments_only(tmp_path, monkeypatch):
+    """A stored measurement stays valid across comment edits, not code edits."""
+    import shutil
+    src = os.path.join(bench.ROOT, "paper_2609_16338_amd", "csrc")
+    dst = tmp_path / "paper_2609_16338_amd" / "csrc"
+    dst.mkdir(parents=True)
+    for name in bench.KERNEL_SOURCES:
+        shutil.copy(os.path.join(src, name), dst / name)
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    h0 = bench.kernel_source_hash()
+    f = dst / "tables.h"
+    f.write_text(f.read_text() + "\n// a comment\n\n")
+    assert bench.kernel_source_hash() == h0
+    f.write_text(f.read_text() + "constexpr int kUnusedForTheHashTest = 1;\n")
+    assert bench.kernel_source_hash() != h0
