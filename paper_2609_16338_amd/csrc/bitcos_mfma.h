@@ -389,14 +389,14 @@ __global__ void __launch_bounds__(mfma_threads(BF16, XS)) bitcos_mfma_kernel(con
     }
 
     // Fetch step t+1.  offn holds the offsets of the unit after step t's:
-    // step t+1's own when it starts a unit.  They are reloaded every step,
-    // unconditionally: loads in a branch into a loop-carried register make
-    // the compiler copy them into place right away, a wait for every load
-    // in flight.
+    // step t+1's own when it starts a unit.
     fs = advance(cs);
 #pragma unroll
     for (int r = 0; r < RT; ++r) nxt.pos[r] = fs.c == 0 ? offn[r] : cur.pos[r] + stot[r];
-    next_unit_offsets(fs.unit, offn);
+    // The unit after step t+1's is read only when step t+1 ends its unit (a
+    // lane-masked branch: loads under a uniform branch into this
+    // loop-carried register would make the compiler copy it into place).
+    if (lane_mask(fs.last)) next_unit_offsets(fs.unit, offn);
     issue(fs, nxt);
 
     // The groups at raised wave priority (as in the batch-1 kernels): int8
