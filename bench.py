@@ -113,10 +113,16 @@ def emit(obj, args):
             f.write(line + "\n")
 
 
-# Sources of the BITCOS kernels: a stored HBM-traffic measurement is reported
-# only while these files are unchanged.
-KERNEL_SOURCES = ["bitcos_diag.h", "bitcos_fast.h", "bitcos_kernel.h", "bitcos_mfma.h", "mfma_common.h", "tables.h",
-                  "device_common.h", "batch.h", "batch.hip", "gemv_bitcos.hip", "launch_common.h", "plan.h"]
+# Sources of each BITCOS kernel (its device code, the launcher that sizes its
+# grid and the batch-table builder): a stored HBM-traffic measurement of a
+# launch is reported only while its kernel's sources are unchanged.
+_COMMON_SOURCES = ["bitcos_kernel.h", "tables.h", "device_common.h", "batch.h", "batch.hip", "launch_common.h",
+                   "plan.h"]
+KERNEL_SOURCES = {
+    "bitcos_fast_kernel": ["bitcos_fast.h", "gemv_bitcos.hip"] + _COMMON_SOURCES,
+    "bitcos_diag_kernel": ["bitcos_diag.h", "bitcos_fast.h", "mfma_common.h", "gemv_bitcos.hip"] + _COMMON_SOURCES,
+    "bitcos_mfma_kernel": ["bitcos_mfma.h", "mfma_common.h", "gemv_bitcos_mfma.hip"] + _COMMON_SOURCES,
+}
 TRAFFIC_FILES = {
     "qwen3_32b_layers": [os.path.join(ROOT, "profiles", f) for f in (
         "bitcos_fast_bf16_qwen3_32b_k5120_traffic.txt", "bitcos_mfma_bf16_qwen3_32b_m16_traffic.txt")],
@@ -125,13 +131,13 @@ TRAFFIC_FILES = {
 COPY_MIB = 256
 
 
-def kernel_source_hash():
-    """Hash of the kernel sources without their // comments and blank space,
+def kernel_source_hash(kernel="bitcos_fast_kernel"):
+    """Hash of a kernel's sources without their // comments and blank space,
     so that editing a comment keeps a stored measurement valid."""
     import hashlib
     import re
     h = hashlib.sha256()
-    for name in KERNEL_SOURCES:
+    for name in KERNEL_SOURCES[kernel]:
         with open(os.path.join(ROOT, "paper_2609_16338_amd", "csrc", name), encoding="utf-8") as f:
             code = re.sub(r"//[^\n]*", "", f.read())
         h.update(name.encode() + b"\0" + " ".join(code.split()).encode())
@@ -151,7 +157,10 @@ def stored_traffic(workload, launch):
         except OSError:
             continue
         kv = {k.strip(): v.strip() for k, v in kv.items()}
-        if kv.get("launch") != launch or kv.get("kernel_source_hash") != kernel_source_hash():
+        kernel = launch.split("<")[0]
+        if kv.get("launch") != launch or kernel not in KERNEL_SOURCES:
+            continue
+        if kv.get("kernel_source_hash") != kernel_source_hash(kernel):
             continue
         try:
             return int(float(kv["traffic_bytes_per_launch"]))
@@ -774,7 +783,8 @@ def profile_pass(args):
     torch.cuda.synchronize()
     alg = sum(e[3].payload_bits / 8 + args.batch * (e[3].k * 2 + e[3].n * 4) for e in top.entries)
     print(f"[profile-pass] {args.workload} dominant launch: {launch_label(top, args.batch)}, "
-          f"algorithmic bytes {int(alg)}; copy {COPY_MIB} MiB; kernel_source_hash {kernel_source_hash()}",
+          f"algorithmic bytes {int(alg)}; copy {COPY_MIB} MiB; "
+          f"kernel_source_hash {kernel_source_hash(launch_label(top, args.batch).split('<')[0])}",
           flush=True)
 
 

@@ -172,7 +172,7 @@ def test_stored_traffic_only_for_the_measured_launch():
     assert bench.stored_traffic("qwen3_32b_layers", f"{other}<{rest}") is None
     assert bench.stored_traffic("qwen3_32b_layers", launch.replace(" GEMVs", "0 GEMVs")) is None
     assert bench.stored_traffic("no_such_set", launch) is None
-    if kv["kernel_source_hash"].strip() == bench.kernel_source_hash():
+    if kv["kernel_source_hash"].strip() == bench.kernel_source_hash(kernel):
         assert bench.stored_traffic("qwen3_32b_layers", launch) == int(float(kv["traffic_bytes_per_launch"]))
 
 
@@ -182,12 +182,17 @@ def test_kernel_source_hash_ignores_comments_only(tmp_path, monkeypatch):
     src = os.path.join(bench.ROOT, "paper_2609_16338_amd", "csrc")
     dst = tmp_path / "paper_2609_16338_amd" / "csrc"
     dst.mkdir(parents=True)
-    for name in bench.KERNEL_SOURCES:
+    for name in {n for names in bench.KERNEL_SOURCES.values() for n in names}:
         shutil.copy(os.path.join(src, name), dst / name)
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
-    h0 = bench.kernel_source_hash()
+    h0 = {k: bench.kernel_source_hash(k) for k in bench.KERNEL_SOURCES}
     f = dst / "tables.h"
     f.write_text(f.read_text() + "\n// a comment\n\n")
-    assert bench.kernel_source_hash() == h0
+    assert {k: bench.kernel_source_hash(k) for k in bench.KERNEL_SOURCES} == h0
+    # a code change in one kernel's own source leaves the others' measurements valid
+    m = dst / "bitcos_mfma.h"
+    m.write_text(m.read_text() + "constexpr int kUnusedForTheHashTest = 1;\n")
+    assert bench.kernel_source_hash("bitcos_mfma_kernel") != h0["bitcos_mfma_kernel"]
+    assert bench.kernel_source_hash("bitcos_fast_kernel") == h0["bitcos_fast_kernel"]
     f.write_text(f.read_text() + "constexpr int kUnusedForTheHashTest = 1;\n")
-    assert bench.kernel_source_hash() != h0
+    assert all(bench.kernel_source_hash(k) != h0[k] for k in bench.KERNEL_SOURCES)
