@@ -230,6 +230,12 @@ __device__ __forceinline__ void build_trit5_bf16(Trit5TablesBf16& tb, int tid, i
   }
 }
 
+// A table entry read as one 16-byte vector.  Its fourth dword is always zero
+// and unused; read through a uint4 the compiler drops it and splits the rest
+// into an 8-byte and a 4-byte read, twice the LDS instructions.
+typedef unsigned u32v4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ u32v4 lds_read16(const uint4* p) { return *reinterpret_cast<const u32v4*>(p); }
+
 // Byte i of the lane's aligned code stream A.
 template <int NA>
 __device__ __forceinline__ uint32_t code_byte(const uint32_t (&A)[NA], int i) {
@@ -346,13 +352,17 @@ __global__ void __launch_bounds__(fixed_threads(false, BF16, BK)) trit5_gemv_ker
       } else {
 #pragma unroll
         for (int c = 0; c < 13; ++c) {
-          const uint4 e0 = tab.t[0][code_byte(A, 26 * t + 2 * c + 0) * kTrit5Copies + cpy];
-          const uint4 e1 = tab.t[1][code_byte(A, 26 * t + 2 * c + 1) * kTrit5Copies + cpy];
+          const u32v4 e0 = lds_read16(&tab.t[0][code_byte(A, 26 * t + 2 * c + 0) * kTrit5Copies + cpy]);
+          const u32v4 e1 = lds_read16(&tab.t[1][code_byte(A, 26 * t + 2 * c + 1) * kTrit5Copies + cpy]);
           acc = bdot2(e0.x, x[5 * c + 0], acc);
           acc = bdot2(e0.y, x[5 * c + 1], acc);
           acc = bdot2(e0.z | e1.x, x[5 * c + 2], acc);
           acc = bdot2(e1.y, x[5 * c + 3], acc);
           if (c < 12) acc = bdot2(e1.z, x[5 * c + 4], acc);  // weights 128, 129 do not exist
+          // Unscheduled, the compiler hoists all 26 table reads of a block
+          // (4 registers each) and the one-block variants spill; a fence every
+          // six pairs bounds the reads in flight.
+          if (c % 6 == 5) __builtin_amdgcn_sched_barrier(0);
         }
       }
       run[t] = acc;
