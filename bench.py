@@ -122,6 +122,8 @@ KERNEL_SOURCES = {
     "bitcos_fast_kernel": ["bitcos_fast.h", "gemv_bitcos.hip"] + _COMMON_SOURCES,
     "bitcos_diag_kernel": ["bitcos_diag.h", "bitcos_fast.h", "mfma_common.h", "gemv_bitcos.hip"] + _COMMON_SOURCES,
     "bitcos_mfma_kernel": ["bitcos_mfma.h", "mfma_common.h", "gemv_bitcos_mfma.hip"] + _COMMON_SOURCES,
+    "trit5_gemv_kernel": ["fixed_kernel.h", "fixed_trit5.hip", "gemv_fixed.hip"] + _COMMON_SOURCES,
+    "bit2_gemv_kernel": ["fixed_kernel.h", "fixed_bit2.hip", "gemv_fixed.hip"] + _COMMON_SOURCES,
 }
 TRAFFIC_FILES = {
     "qwen3_32b_layers": [os.path.join(ROOT, "profiles", f) for f in (

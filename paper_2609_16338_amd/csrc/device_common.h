@@ -107,22 +107,44 @@ __device__ __forceinline__ int dpp_i(int v) {
   return __builtin_amdgcn_update_dpp(0, v, CTRL, ROWS, 0xF, false);
 }
 
-template <int SEG>
-__device__ __forceinline__ int seg_sum(int v) {
-  static_assert(SEG == 2 || SEG == 4 || SEG == 8 || SEG == 16 || SEG == 32 || SEG == 64, "segment");
-  if constexpr (SEG == 8) v += dpp_i<0x141>(v);  // row_half_mirror
-  if constexpr (SEG <= 8) {
-    v += dpp_i<0xB1>(v);                          // quad_perm [1,0,3,2]
-    if constexpr (SEG >= 4) v += dpp_i<0x4E>(v);  // quad_perm [2,3,0,1]
-  } else {
-    v += dpp_i<0x128>(v);  // row_ror:8
-    v += dpp_i<0x124>(v);  // row_ror:4
-    v += dpp_i<0x122>(v);  // row_ror:2
-    v += dpp_i<0x121>(v);  // row_ror:1
-    if constexpr (SEG >= 32) v += dpp_i<0x142, 0xA>(v);  // row_bcast:15 into rows 1, 3
-    if constexpr (SEG == 64) v += dpp_i<0x143, 0x8>(v);  // row_bcast:31 into row 3
+// Segments of a width that is not a power of two (SEG lanes from lane
+// SEG * r) do not line up with DPP rows: lane j of a segment adds the value
+// of the lane d below it, for d = 1, 2, 4, ... < SEG, where j >= d (lane moves
+// through ds_bpermute, which touches no LDS memory).  After the last round
+// lane j holds the sum of the segment's lanes max(0, j - 2^r + 1) .. j, so the
+// last lane holds the whole segment's sum, as above.
+template <int SEG, class T>
+__device__ __forceinline__ T seg_sum_any(T v) {
+  const int lane = static_cast<int>(__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u)));
+  const int j = lane % SEG;
+#pragma unroll
+  for (int d = 1; d < SEG; d <<= 1) {
+    const int o = __builtin_amdgcn_ds_bpermute(((lane - d) & 63) << 2, __builtin_bit_cast(int, v));
+    v += j >= d ? __builtin_bit_cast(T, o) : T(0);
   }
   return v;
+}
+
+template <int SEG>
+__device__ __forceinline__ int seg_sum(int v) {
+  if constexpr (SEG & (SEG - 1)) {
+    return seg_sum_any<SEG>(v);
+  } else {
+    static_assert(SEG == 2 || SEG == 4 || SEG == 8 || SEG == 16 || SEG == 32 || SEG == 64, "segment");
+    if constexpr (SEG == 8) v += dpp_i<0x141>(v);  // row_half_mirror
+    if constexpr (SEG <= 8) {
+      v += dpp_i<0xB1>(v);                          // quad_perm [1,0,3,2]
+      if constexpr (SEG >= 4) v += dpp_i<0x4E>(v);  // quad_perm [2,3,0,1]
+    } else {
+      v += dpp_i<0x128>(v);  // row_ror:8
+      v += dpp_i<0x124>(v);  // row_ror:4
+      v += dpp_i<0x122>(v);  // row_ror:2
+      v += dpp_i<0x121>(v);  // row_ror:1
+      if constexpr (SEG >= 32) v += dpp_i<0x142, 0xA>(v);  // row_bcast:15 into rows 1, 3
+      if constexpr (SEG == 64) v += dpp_i<0x143, 0x8>(v);  // row_bcast:31 into row 3
+    }
+    return v;
+  }
 }
 
 template <int CTRL, int ROWS = 0xF>
@@ -132,20 +154,24 @@ __device__ __forceinline__ float dpp_f(float v) {
 
 template <int SEG>
 __device__ __forceinline__ float seg_sum(float v) {
-  static_assert(SEG == 2 || SEG == 4 || SEG == 8 || SEG == 16 || SEG == 32 || SEG == 64, "segment");
-  if constexpr (SEG == 8) v += dpp_f<0x141>(v);
-  if constexpr (SEG <= 8) {
-    v += dpp_f<0xB1>(v);
-    if constexpr (SEG >= 4) v += dpp_f<0x4E>(v);
+  if constexpr (SEG & (SEG - 1)) {
+    return seg_sum_any<SEG>(v);
   } else {
-    v += dpp_f<0x128>(v);
-    v += dpp_f<0x124>(v);
-    v += dpp_f<0x122>(v);
-    v += dpp_f<0x121>(v);
-    if constexpr (SEG >= 32) v += dpp_f<0x142, 0xA>(v);
-    if constexpr (SEG == 64) v += dpp_f<0x143, 0x8>(v);
+    static_assert(SEG == 2 || SEG == 4 || SEG == 8 || SEG == 16 || SEG == 32 || SEG == 64, "segment");
+    if constexpr (SEG == 8) v += dpp_f<0x141>(v);
+    if constexpr (SEG <= 8) {
+      v += dpp_f<0xB1>(v);
+      if constexpr (SEG >= 4) v += dpp_f<0x4E>(v);
+    } else {
+      v += dpp_f<0x128>(v);
+      v += dpp_f<0x124>(v);
+      v += dpp_f<0x122>(v);
+      v += dpp_f<0x121>(v);
+      if constexpr (SEG >= 32) v += dpp_f<0x142, 0xA>(v);
+      if constexpr (SEG == 64) v += dpp_f<0x143, 0x8>(v);
+    }
+    return v;
   }
-  return v;
 }
 
 __device__ __forceinline__ uint32_t bytes4(uint32_t b0, uint32_t b1, uint32_t b2, uint32_t b3) {

@@ -6,11 +6,12 @@
 
 namespace bitcos {
 
-// A GEMV wave covers `rows` = 64 / seg rows per step.  Each row is split over
-// `lanes` <= seg lanes; every lane owns `per_lane` consecutive units of the
-// row (32-weight words for BITCOS, 128-weight blocks for five-trit, 16-weight
-// words for 2-bit).  `seg` is a power of two so a row's partial sums reduce
-// with butterflies inside an aligned lane segment.
+// A GEMV wave covers `rows` = 64 / seg rows per step (rounded down).  Each row
+// is split over `lanes` <= seg lanes; every lane owns `per_lane` consecutive
+// units of the row (32-weight words for BITCOS, 128-weight blocks for
+// five-trit, 16-weight words for 2-bit).  `seg` is a power of two, so a row's
+// partial sums reduce with butterflies inside an aligned lane segment, except
+// for the five-trit bf16 kernel's 20-lane segment (three rows, 60 lanes).
 struct Tile {
   int per_lane = 0;
   int seg = 0;
@@ -26,19 +27,24 @@ constexpr int kMaxBlocksBf16 = 2;  // five-trit: 64 dwords per block
 constexpr int kMaxWords2I8 = 32;   // 2-bit: 4 dwords per 16-weight word
 constexpr int kMaxWords2Bf16 = 16; // 2-bit: 8 dwords per word
 
-// Pick the tile that leaves the fewest lanes idle for `units_per_row` units
-// split into chunks of at most `max_per_lane`; ties go to the smaller
-// per-lane count (fewer registers), or with `wide` to the larger one (more
-// rows per wave step).  Returns false if no tile fits.
-inline bool choose_tile(int units_per_row, int max_per_lane, Tile* t, bool wide = false) {
+// Pick the tile that leaves the fewest lanes of the wave idle for
+// `units_per_row` units split into chunks of at most `max_per_lane`; ties go
+// to the smaller per-lane count (fewer registers), or with `wide` to the
+// larger one (more rows per wave step).  `seg20` also offers the 20-lane
+// segment: the five-trit bf16 kernel holds at most two blocks' activations
+// per lane, so rows of 20 or 40 blocks (K = 2560, 5120) would otherwise leave
+// 3/8 of the lanes idle.  Returns false if no tile fits.
+inline bool choose_tile(int units_per_row, int max_per_lane, Tile* t, bool wide = false, bool seg20 = false) {
   double best = -1.0;
   Tile pick;
-  for (int seg = 64; seg >= 4; seg /= 2) {
+  constexpr int kSegs[6] = {64, 32, 20, 16, 8, 4};
+  for (int seg : kSegs) {
+    if (seg == 20 && !seg20) continue;
     int per_lane = (units_per_row + seg - 1) / seg;
     if (per_lane < 1) per_lane = 1;
     if (per_lane > max_per_lane) continue;
     int lanes = (units_per_row + per_lane - 1) / per_lane;
-    double util = double(units_per_row) / double(seg * per_lane);
+    double util = double(units_per_row) * double(64 / seg) / double(64 * per_lane);
     bool better = util > best + 1e-12 ||
                   (util > best - 1e-12 && (wide ? per_lane > pick.per_lane : per_lane < pick.per_lane));
     if (better) {
