@@ -511,24 +511,36 @@ __global__ void __launch_bounds__(fixed_threads(true, BF16, WB)) bit2_gemv_kerne
     Acc acc = Acc(0);
     // The decode burst at raised wave priority, as in the BITCOS kernels.
     __builtin_amdgcn_s_setprio(1);
+    if constexpr (!BF16) {
 #pragma unroll
-    for (int w = 0; w < WB; ++w) {
-      const uint32_t c = cw0[w];
-      if constexpr (!BF16) {
+      for (int w = 0; w < WB; ++w) {
+        const uint32_t c = cw0[w];
         acc -= xsum[w];
         acc = sdot4(c & 0x03030303u, xr[w][0], acc);
         acc = sdot4((c >> 2) & 0x03030303u, xr[w][1], acc);
         acc = sdot4((c >> 4) & 0x03030303u, xr[w][2], acc);
         acc = sdot4((c >> 6) & 0x03030303u, xr[w][3], acc);
-      } else {
+        run[w] = acc;
+      }
+    } else {
+      // The next word's four lookups are issued before this word's products,
+      // so a word waits on lookups issued a word earlier, not just before use.
+      auto look = [&](uint32_t c, uint2 (&e)[4]) {
+#pragma unroll
+        for (int b = 0; b < 4; ++b) e[b] = tab.t[((c >> (8 * b)) & 0xFFu) * kBit2Copies + cpy];
+      };
+      uint2 e[2][4];
+      look(cw0[0], e[0]);
+#pragma unroll
+      for (int w = 0; w < WB; ++w) {
+        if (w + 1 < WB) look(cw0[w + 1], e[(w + 1) & 1]);
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
-          const uint2 e = tab.t[((c >> (8 * b)) & 0xFFu) * kBit2Copies + cpy];
-          acc = bdot2(e.x, xr[w][2 * b + 0], acc);
-          acc = bdot2(e.y, xr[w][2 * b + 1], acc);
+          acc = bdot2(e[w & 1][b].x, xr[w][2 * b + 0], acc);
+          acc = bdot2(e[w & 1][b].y, xr[w][2 * b + 1], acc);
         }
+        run[w] = acc;
       }
-      run[w] = acc;
     }
     __builtin_amdgcn_s_setprio(0);
     finish_row<SEG, BF16, WB, 8>(mode, ydst, ybytes, run, row, live, j, ph, xs, SC0, tensor_scale);
