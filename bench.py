@@ -102,6 +102,9 @@ def parse(argv=None):
                     help="plain streaming-read bandwidth of this GPU (own JSON line)")
     ap.add_argument("--sweep-copies", type=int, default=40,
                     help="device copies of each swept matrix streamed per launch (> 2 x the 256 MB Infinity Cache)")
+    ap.add_argument("--sweep-shape", default="8192x8192",
+                    help="N x K of the swept matrix (the paper's own sweep matrix is 32768x16384)")
+    ap.add_argument("--sweep-z", default="", help="comma-separated zero densities (default: the five of the sweep and 0.95)")
     return ap.parse_args(argv)
 
 
@@ -859,24 +862,38 @@ def hbm_read(args):
           "rates_GBs": res}, args)
 
 
+def sweep_points(args):
+    """(n, k, [(z index, z)]) of the sweep: `--sweep-shape` N x K (multiples of
+    128) and the `--sweep-z` densities, by default the five of the sweep and
+    the paper's extreme 0.95; a z of the sweep keeps its seed index."""
+    n, k = (int(v) for v in args.sweep_shape.lower().split("x"))
+    if n < 1 or k < 128 or k % 128:
+        raise SystemExit(f"--sweep-shape {args.sweep_shape}: N >= 1 and K a multiple of 128")
+    allz = wl.SWEEP_Z + (0.95,)
+    zs = [float(v) for v in args.sweep_z.split(",") if v] if args.sweep_z else list(allz)
+    return n, k, [(allz.index(z) if z in allz else len(allz) + i, z) for i, z in enumerate(zs)]
+
+
 def sweep(args):
-    """Zero-density sweep: one 8192 x 8192 matrix with group-128 scales per z,
-    batch 1, BITCOS against the five-trit and 2-bit kernels on this GPU.  Each
-    format's blob is copied `--sweep-copies` times in HBM and one persistent
-    launch covers all copies, so every launch streams more than twice the
-    Infinity Cache; time per GEMV = launch time / copies."""
+    """Zero-density sweep: one N x K matrix (8192 x 8192 by default) with
+    group-128 scales per z, batch 1, BITCOS against the five-trit and 2-bit
+    kernels on this GPU.  Each format's blob is copied `--sweep-copies` times
+    in HBM and one persistent launch covers all copies, so every launch
+    streams more than twice the Infinity Cache; time per GEMV = launch time /
+    copies."""
     import torch
 
     from paper_2609_16338_amd import _native as N
     from paper_2609_16338_amd import api
 
-    cid, k = 4, 8192
+    cid = 4
+    n, k, zpts = sweep_points(args)
     xi = torch.from_numpy(wl.activation_inputs(cid, "int8", 1, k)).cuda().reshape(-1)
     xb = torch.from_numpy(wl.activation_inputs(cid, "bf16", 1, k).view(np.int16)).view(torch.bfloat16).cuda().reshape(-1)
     names = {N.FMT_BITCOS: "bitcos", N.FMT_TRIT5: "trit5", N.FMT_BIT2: "bit2"}
     rows = []
-    for zi, z in enumerate(wl.SWEEP_Z + (0.95,)):  # the paper's extreme point beside the config's five
-        spec = wl.sweep_spec(z)
+    for zi, z in zpts:
+        spec = wl.sweep_spec(z, n, k)
         w, sc = wl.matrix_inputs(cid, 0, zi, spec)
         row = {"z": z, "z_measured": round(float((w == 0).mean()), 5)}
         for fmt, nm in names.items():
@@ -916,7 +933,7 @@ def sweep(args):
         return None
 
     emit({
-        "metric": "zero-density sweep, 8192x8192 g128, batch 1: per-GEMV time, effective GB/s, speedups",
+        "metric": f"zero-density sweep, {n}x{k} g128, batch 1: per-GEMV time, effective GB/s, speedups",
         "unit": "us",
         "copies_per_launch": args.sweep_copies,
         "steps": args.steps,

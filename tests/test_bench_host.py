@@ -9,6 +9,7 @@ import pytest
 
 torch = pytest.importorskip("torch")
 import bench  # noqa: E402
+import workloads as wl  # noqa: E402
 
 
 class _FakeGraph:
@@ -196,3 +197,18 @@ def test_kernel_source_hash_ignores_comments_only(tmp_path, monkeypatch):
     assert bench.kernel_source_hash("bitcos_fast_kernel") == h0["bitcos_fast_kernel"]
     f.write_text(f.read_text() + "constexpr int kUnusedForTheHashTest = 1;\n")
     assert all(bench.kernel_source_hash(k) != h0[k] for k in bench.KERNEL_SOURCES)
+
+
+def test_sweep_points():
+    """The sweep's shape and densities: the default 8192 x 8192 over the five
+    densities and 0.95, or a given shape and list; a density of the sweep keeps
+    its seed index, others get new ones."""
+    n, k, pts = bench.sweep_points(bench.parse(["--sweep"]))
+    assert (n, k) == (8192, 8192)
+    assert pts == list(enumerate(wl.SWEEP_Z + (0.95,)))
+    n, k, pts = bench.sweep_points(bench.parse(["--sweep", "--sweep-shape", "32768x16384", "--sweep-z", "0.42,0.6"]))
+    assert (n, k) == (32768, 16384)
+    assert pts == [(wl.SWEEP_Z.index(0.42), 0.42), (len(wl.SWEEP_Z) + 2, 0.6)]
+    with pytest.raises(SystemExit):
+        bench.sweep_points(bench.parse(["--sweep", "--sweep-shape", "100x100"]))
+

@@ -142,9 +142,10 @@ WORKLOADS = {
 SWEEP_Z = (0.30, 0.375, 0.42, 0.467, 0.515)
 
 
-def sweep_spec(z: float) -> MatrixSpec:
-    """One 8192 x 8192 matrix of the zero-density sweep (g128, int8 x)."""
-    return MatrixSpec(f"sweep_z{z}", 8192, 8192, z, 128, 0.01, 0.1)
+def sweep_spec(z: float, n: int = 8192, k: int = 8192) -> MatrixSpec:
+    """One matrix of the zero-density sweep (g128, int8 x): 8192 x 8192, or
+    another shape such as the paper's 32768 x 16384 sweep matrix."""
+    return MatrixSpec(f"sweep_z{z}", n, k, z, 128, 0.01, 0.1)
 
 
 def matrix_inputs(cid: int, layer: int, midx: int, spec: MatrixSpec):
