@@ -125,6 +125,42 @@ def test_bf16_all_formats(k, group):
         check_bf16(y, ref, bound)
 
 
+@pytest.mark.parametrize("k", [2560, 5120])
+def test_trit5_bf16_twenty_lane_segments_multi_step(k):
+    """Five-trit with bf16 activations on rows of 20 or 40 blocks runs 20-lane
+    segments: three rows per wave step, the row's partial sums moved by
+    ds_bpermute rounds, the last four lanes idle.  One GEMV with more steps
+    than twice the most waves the GPU holds, so every wave of the persistent
+    grid takes several; the row count leaves the last step one row short.
+    Sampled rows (and the first and last) against the oracle; two runs give
+    identical bits."""
+    from parity_checks import sampled_rows
+    p = torch.cuda.get_device_properties(0)
+    resident = p.multi_processor_count * max(p.max_threads_per_multi_processor // 64, 1)
+    n = 3 * 2 * resident + 2
+    w, sc = inputs(n, k, 0.42, 128, 78)
+    xb = wl.act_bf16(1, k, wl.rng_for(98, k))
+    L, blob = api.plan_and_pack(N.FMT_TRIT5, w, sc, 128)
+    info = api.describe(L, 1, N.X_BF16)
+    assert (info.seg_lanes, info.rows_per_step, info.per_lane) == (20, 3, k // 2560)
+    assert info.waves > 2 * resident
+    say("trit5 bf16 20-lane", n, k, info.waves)
+    blob_d = torch.from_numpy(blob).cuda()
+    xd = torch.from_numpy(xb.view(np.int16)).view(torch.bfloat16).cuda().reshape(-1)
+    outs = []
+    for _ in range(2):
+        y = torch.full((n,), float("nan"), dtype=torch.float32, device="cuda")
+        api.gemv(L, blob_d, xd, y)
+        torch.cuda.synchronize()
+        outs.append(y.cpu().numpy())
+    assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))
+    assert np.all(np.isfinite(outs[0]))
+    rows = sampled_rows(n, 300, k)
+    scr = sc.reshape(n, -1)[rows].reshape(-1)
+    ref = O.dense_gemv(w[rows], scr, 128, xb, x_is_bf16_bits=True)
+    check_bf16(outs[0][rows][None], ref, bf16_bound(w[rows], scr, 128, xb))
+
+
 def test_bf16_unsupported_shape_is_an_error_not_a_fallback():
     # Rows too long for the batch-1 tiles with two rows per sign offset: the
     # small-batch kernel needs one offset per row, so no kernel takes it.
