@@ -318,8 +318,7 @@ int bitcos_pack_device_noalloc(const int8_t* w_dev, const uint16_t* scales_dev, 
 typedef struct bitcos_launch_info {
   int32_t per_lane;        /* BITCOS: 32-weight words per lane; TRIT5: 128-blocks; BIT2: 16-weight words */
   int32_t seg_lanes;       /* lanes that share one row: a power of two, or 20
-                              (five-trit with bf16 activations, rows of 20 or
-                              40 blocks)                                       */
+                              (five-trit, rows of 20 or 40 blocks)             */
   int32_t rows_per_step;   /* rows a wave covers per step = 64 / seg_lanes,
                               rounded down                                     */
   int32_t lanes_used;      /* lanes per row that hold weights                   */

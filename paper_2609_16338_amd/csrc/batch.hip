@@ -18,7 +18,7 @@ int tile_for(const bitcos_layout* L, int32_t x_dtype, int* per_lane, int* seg, i
   bool ok;
   switch (L->format) {
     case BITCOS_FMT_BITCOS: ok = bitcos_tile(L->k, bf16, &t); break;
-    case BITCOS_FMT_TRIT5: ok = choose_tile(L->k / 128, bf16 ? kMaxBlocksBf16 : kMaxBlocksI8, &t, false, bf16); break;
+    case BITCOS_FMT_TRIT5: ok = choose_tile(L->k / 128, bf16 ? kMaxBlocksBf16 : kMaxBlocksI8, &t, false, true); break;
     case BITCOS_FMT_BIT2: ok = choose_tile(L->k / 16, bf16 ? kMaxWords2Bf16 : kMaxWords2I8, &t); break;
     default: return BITCOS_E_ARG;
   }

@@ -3,9 +3,13 @@
 
 namespace fixed_k {
 KernelFn pick_trit5(int per_lane, int seg, bool bf16, bool table) {
-  if (bf16 && seg == 20) {
-    const auto seq = std::make_integer_sequence<int, bitcos::kMaxBlocksBf16>{};
-    return table ? pick_p<Trit5K, 20, true, true>(per_lane, seq) : pick_p<Trit5K, 20, true, false>(per_lane, seq);
+  if (seg == 20) {
+    if (bf16) {
+      const auto seq = std::make_integer_sequence<int, bitcos::kMaxBlocksBf16>{};
+      return table ? pick_p<Trit5K, 20, true, true>(per_lane, seq) : pick_p<Trit5K, 20, true, false>(per_lane, seq);
+    }
+    const auto seq = std::make_integer_sequence<int, bitcos::kMaxBlocksI8>{};
+    return table ? pick_p<Trit5K, 20, false, true>(per_lane, seq) : pick_p<Trit5K, 20, false, false>(per_lane, seq);
   }
   if (bf16)
     return table ? pick_kernel<Trit5K, bitcos::kMaxBlocksBf16, true, true>(per_lane, seg)

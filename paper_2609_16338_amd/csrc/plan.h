@@ -11,7 +11,7 @@ namespace bitcos {
 // units of the row (32-weight words for BITCOS, 128-weight blocks for
 // five-trit, 16-weight words for 2-bit).  `seg` is a power of two, so a row's
 // partial sums reduce with butterflies inside an aligned lane segment, except
-// for the five-trit bf16 kernel's 20-lane segment (three rows, 60 lanes).
+// for the five-trit kernel's 20-lane segment (three rows, 60 lanes).
 struct Tile {
   int per_lane = 0;
   int seg = 0;
@@ -22,7 +22,7 @@ struct Tile {
 // Largest per-lane count that has a compiled kernel, by activation type.
 constexpr int kMaxWordsI8 = 16;    // BITCOS: x in VGPRs, 8 dwords per 32-weight word
 constexpr int kMaxWordsBf16 = 8;   // BITCOS: 16 dwords per word
-constexpr int kMaxBlocksI8 = 5;    // five-trit: 32 dwords per 128-weight block
+constexpr int kMaxBlocksI8 = 4;    // five-trit: 32 dwords per 128-weight block (five blocks spill)
 constexpr int kMaxBlocksBf16 = 2;  // five-trit: 64 dwords per block
 constexpr int kMaxWords2I8 = 32;   // 2-bit: 4 dwords per 16-weight word
 constexpr int kMaxWords2Bf16 = 16; // 2-bit: 8 dwords per word
@@ -31,9 +31,10 @@ constexpr int kMaxWords2Bf16 = 16; // 2-bit: 8 dwords per word
 // `units_per_row` units split into chunks of at most `max_per_lane`; ties go
 // to the smaller per-lane count (fewer registers), or with `wide` to the
 // larger one (more rows per wave step).  `seg20` also offers the 20-lane
-// segment: the five-trit bf16 kernel holds at most two blocks' activations
-// per lane, so rows of 20 or 40 blocks (K = 2560, 5120) would otherwise leave
-// 3/8 of the lanes idle.  Returns false if no tile fits.
+// segment: the five-trit kernel holds at most two (bf16) or four (int8)
+// blocks' activations per lane, so rows of 20 or 40 blocks (K = 2560, 5120)
+// would otherwise leave up to 3/8 of the lanes idle.  Returns false if no
+// tile fits.
 inline bool choose_tile(int units_per_row, int max_per_lane, Tile* t, bool wide = false, bool seg20 = false) {
   double best = -1.0;
   Tile pick;

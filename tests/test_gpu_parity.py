@@ -126,39 +126,51 @@ def test_bf16_all_formats(k, group):
 
 
 @pytest.mark.parametrize("k", [2560, 5120])
-def test_trit5_bf16_twenty_lane_segments_multi_step(k):
-    """Five-trit with bf16 activations on rows of 20 or 40 blocks runs 20-lane
-    segments: three rows per wave step, the row's partial sums moved by
-    ds_bpermute rounds, the last four lanes idle.  One GEMV with more steps
-    than twice the most waves the GPU holds, so every wave of the persistent
-    grid takes several; the row count leaves the last step one row short.
-    Sampled rows (and the first and last) against the oracle; two runs give
+@pytest.mark.parametrize("kind", ["bf16", "int8"])
+def test_trit5_twenty_lane_segments_multi_step(kind, k):
+    """Five-trit on rows of 20 or 40 blocks runs 20-lane segments: three rows
+    per wave step, the row's partial sums moved by ds_bpermute rounds, the
+    last four lanes idle.  One GEMV with more steps than twice the most waves
+    the GPU holds, so every wave of the persistent grid takes several; the row
+    count leaves the last step one row short.  Sampled rows (and the first and
+    last) against the oracle (int8: raw int32 sums, bit-exact); two runs give
     identical bits."""
     from parity_checks import sampled_rows
     p = torch.cuda.get_device_properties(0)
     resident = p.multi_processor_count * max(p.max_threads_per_multi_processor // 64, 1)
     n = 3 * 2 * resident + 2
     w, sc = inputs(n, k, 0.42, 128, 78)
-    xb = wl.act_bf16(1, k, wl.rng_for(98, k))
+    if kind == "bf16":
+        x = wl.act_bf16(1, k, wl.rng_for(98, k))
+        xd = torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).cuda().reshape(-1)
+    else:
+        x = wl.act_int8(1, k, wl.rng_for(99, k))
+        xd = torch.from_numpy(x).cuda().reshape(-1)
     L, blob = api.plan_and_pack(N.FMT_TRIT5, w, sc, 128)
-    info = api.describe(L, 1, N.X_BF16)
+    info = api.describe(L, 1, N.X_BF16 if kind == "bf16" else N.X_I8)
     assert (info.seg_lanes, info.rows_per_step, info.per_lane) == (20, 3, k // 2560)
     assert info.waves > 2 * resident
-    say("trit5 bf16 20-lane", n, k, info.waves)
+    say("trit5 20-lane", kind, n, k, info.waves)
     blob_d = torch.from_numpy(blob).cuda()
-    xd = torch.from_numpy(xb.view(np.int16)).view(torch.bfloat16).cuda().reshape(-1)
+    y_mode = N.Y_F32 if kind == "bf16" else N.Y_I32_RAW
     outs = []
     for _ in range(2):
-        y = torch.full((n,), float("nan"), dtype=torch.float32, device="cuda")
-        api.gemv(L, blob_d, xd, y)
+        if kind == "bf16":
+            y = torch.full((n,), float("nan"), dtype=torch.float32, device="cuda")
+        else:
+            y = torch.full((n,), -7, dtype=torch.int32, device="cuda")
+        api.gemv(L, blob_d, xd, y, None, y_mode)
         torch.cuda.synchronize()
         outs.append(y.cpu().numpy())
     assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))
-    assert np.all(np.isfinite(outs[0]))
     rows = sampled_rows(n, 300, k)
+    if kind == "int8":
+        assert np.array_equal(outs[0][rows].astype(np.int64), O.dense_gemv_raw(w[rows], x)[0])
+        return
+    assert np.all(np.isfinite(outs[0]))
     scr = sc.reshape(n, -1)[rows].reshape(-1)
-    ref = O.dense_gemv(w[rows], scr, 128, xb, x_is_bf16_bits=True)
-    check_bf16(outs[0][rows][None], ref, bf16_bound(w[rows], scr, 128, xb))
+    ref = O.dense_gemv(w[rows], scr, 128, x, x_is_bf16_bits=True)
+    check_bf16(outs[0][rows][None], ref, bf16_bound(w[rows], scr, 128, x))
 
 
 def test_bf16_unsupported_shape_is_an_error_not_a_fallback():

@@ -156,7 +156,7 @@ def qwen32_set():
     wk = wl.WORKLOADS["qwen3_32b_layers"]
     # Every launch of the batch-1 and M = 16 steps exceeds twice the resident
     # waves: the smallest are the phases that add the down projections' later
-    # column blocks (five-trit int8: 8-row steps, layers x 640 units).
+    # column blocks (five-trit: 3-row steps, layers x 1707 units).
     layers = 26
     samples = {}
     say("building the Qwen3-32B-like set:", layers, "layers, 3 formats")

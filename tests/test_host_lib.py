@@ -231,13 +231,14 @@ def test_describe_tiles():
 
 
 def test_describe_trit5_tiles():
-    # five-trit: at most 5 blocks per lane with int8 activations, 2 with bf16;
-    # bf16 rows of 20 or 40 blocks take the 20-lane segment (3 rows, 60 lanes)
+    # five-trit: at most 4 blocks per lane with int8 activations, 2 with bf16;
+    # rows of 20 or 40 blocks take the 20-lane segment (3 rows, 60 lanes)
     for k, kind, per_lane, seg, rows in [(2560, N.X_BF16, 1, 20, 3), (5120, N.X_BF16, 2, 20, 3),
                                          (4096, N.X_BF16, 1, 32, 2), (12288, N.X_BF16, 2, 64, 1),
                                          (6912, N.X_BF16, 1, 64, 1), (1280, N.X_BF16, 1, 16, 4),
-                                         (2560, N.X_I8, 5, 4, 16), (5120, N.X_I8, 5, 8, 8),
-                                         (6912, N.X_I8, 1, 64, 1)]:
+                                         (2560, N.X_I8, 1, 20, 3), (5120, N.X_I8, 2, 20, 3),
+                                         (4096, N.X_I8, 1, 32, 2), (12288, N.X_I8, 3, 32, 2),
+                                         (6912, N.X_I8, 1, 64, 1), (16384, N.X_I8, 2, 64, 1)]:
         L = api.trit5_plan(np.zeros((8, k), np.int8), 128)
         info = api.describe(L, 1, kind)
         assert (info.per_lane, info.seg_lanes, info.rows_per_step) == (per_lane, seg, rows), (k, kind)
