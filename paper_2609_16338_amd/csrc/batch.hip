@@ -19,7 +19,10 @@ int tile_for(const bitcos_layout* L, int32_t x_dtype, int* per_lane, int* seg, i
   switch (L->format) {
     case BITCOS_FMT_BITCOS: ok = bitcos_tile(L->k, bf16, &t); break;
     case BITCOS_FMT_TRIT5: ok = choose_tile(L->k / 128, bf16 ? kMaxBlocksBf16 : kMaxBlocksI8, &t, false, true); break;
-    case BITCOS_FMT_BIT2: ok = choose_tile(L->k / 16, bf16 ? kMaxWords2Bf16 : kMaxWords2I8, &t); break;
+    case BITCOS_FMT_BIT2:
+      ok = (!bf16 && choose_tile(L->k / 16, kSoftWords2I8, &t)) ||
+           choose_tile(L->k / 16, bf16 ? kMaxWords2Bf16 : kMaxWords2I8, &t);
+      break;
     default: return BITCOS_E_ARG;
   }
   if (!ok) return BITCOS_E_UNSUPPORTED;

@@ -25,6 +25,11 @@ constexpr int kMaxWordsBf16 = 8;   // BITCOS: 16 dwords per word
 constexpr int kMaxBlocksI8 = 4;    // five-trit: 32 dwords per 128-weight block (five blocks spill)
 constexpr int kMaxBlocksBf16 = 2;  // five-trit: 64 dwords per block
 constexpr int kMaxWords2I8 = 32;   // 2-bit: 4 dwords per 16-weight word
+// 2-bit with int8 activations takes at most this many words per lane when a
+// tile fits (27 words at K = 6912 hold about 250 registers, two waves per
+// SIMD, and measured 6 % slower per BitNet-like step than 7 words), and up to
+// kMaxWords2I8 only for rows no such tile covers.
+constexpr int kSoftWords2I8 = 16;
 constexpr int kMaxWords2Bf16 = 16; // 2-bit: 8 dwords per word
 
 // Pick the tile that leaves the fewest lanes of the wave idle for

@@ -246,6 +246,19 @@ def test_describe_trit5_tiles():
         assert info.waves == -(-8 // rows)
 
 
+def test_describe_bit2_tiles():
+    # 2-bit: int8 up to 16 words per lane where a tile fits, else up to 32;
+    # bf16 up to 16
+    for k, kind, per_lane, seg in [(6912, N.X_I8, 7, 64), (6912, N.X_BF16, 7, 64), (16384, N.X_I8, 16, 64),
+                                   (25600, N.X_I8, 25, 64), (5120, N.X_I8, 5, 64), (12288, N.X_BF16, 12, 64)]:
+        L = api.bit2_plan(np.zeros((8, k), np.int8), 128)
+        info = api.describe(L, 1, kind)
+        assert (info.per_lane, info.seg_lanes) == (per_lane, seg), (k, kind)
+    L = api.bit2_plan(np.zeros((8, 32768 + 128), np.int8), 128)
+    with pytest.raises(N.BitcosError):
+        api.describe(L, 1, N.X_I8)
+
+
 def test_describe_kernel_choice():
     """Which kernel a batch-1 call on a layout runs (the launcher's rule)."""
     def kind(group, unit_rows, k=2560, fmt=N.FMT_BITCOS, m=1, x=N.X_BF16):
