@@ -36,7 +36,8 @@ activation bytes + 4 M N output bytes per GEMV) per launch time, against the
 scaled by a plain copy's counters, stored under profiles/) while the kernel
 sources are unchanged; two_term: the launch's time and its bytes at peak HBM
 bandwidth in CU-cycles per 32 weights at the nominal 2.4 GHz, and which
-term is larger.  cpu_baseline: the oracle's decode + dense GEMV on whole
+term is larger; valu: the launch's stored VALU instruction count (rocprofv3
+SQ_INSTS_VALU, same source rule) as a share of the SIMDs' issue cycles.  cpu_baseline: the oracle's decode + dense GEMV on whole
 layer-0 matrices on the host (about 12 s of work).
 
 Other modes print their own JSON line: --sweep (zero-density sweep on one
@@ -133,6 +134,9 @@ TRAFFIC_FILES = {
         "bitcos_fast_bf16_qwen3_32b_k5120_traffic.txt", "bitcos_mfma_bf16_qwen3_32b_m16_traffic.txt")],
     "bitnet2b_layers": [os.path.join(ROOT, "profiles", "bitcos_diag_bf16_bitnet2b_k2560_traffic.txt")],
 }
+COUNTER_FILES = {
+    "qwen3_32b_layers": [os.path.join(ROOT, "profiles", "bitcos_fast_bf16_qwen3_32b_counters.txt")],
+}
 COPY_MIB = 256
 
 
@@ -149,13 +153,10 @@ def kernel_source_hash(kernel="bitcos_fast_kernel"):
     return h.hexdigest()[:16]
 
 
-def stored_traffic(workload, launch):
-    """HBM bytes per launch of the dominant launch from the FETCH_SIZE / WRITE_SIZE
-    passes (scaled by the copy calibration): from the stored measurement of
-    the same launch (`launch`: its label, say "bitcos_fast_kernel<5,32,bf16,
-    table>: 448 GEMVs in one launch"), or None if there is none or the kernel
-    sources changed since it was taken."""
-    for path in TRAFFIC_FILES.get(workload, []):
+def _stored(files, launch):
+    """key: value lines of the first stored measurement of `launch` whose
+    kernel sources are unchanged, or None."""
+    for path in files:
         try:
             with open(path) as f:
                 kv = dict(line.split(":", 1) for line in f if ":" in line and not line.startswith("#"))
@@ -167,11 +168,33 @@ def stored_traffic(workload, launch):
             continue
         if kv.get("kernel_source_hash") != kernel_source_hash(kernel):
             continue
-        try:
-            return int(float(kv["traffic_bytes_per_launch"]))
-        except (KeyError, ValueError):
-            return None
+        return kv
     return None
+
+
+def stored_valu(workload, launch):
+    """VALU instructions per launch of the dominant launch (rocprofv3
+    SQ_INSTS_VALU, wave instructions summed over the GPU) from the stored
+    counter passes of the same launch, or None if there are none or the
+    kernel sources changed since."""
+    kv = _stored(COUNTER_FILES.get(workload, []), launch)
+    try:
+        return None if kv is None else int(float(kv["sq_insts_valu_per_launch"]))
+    except (KeyError, ValueError):
+        return None
+
+
+def stored_traffic(workload, launch):
+    """HBM bytes per launch of the dominant launch from the FETCH_SIZE / WRITE_SIZE
+    passes (scaled by the copy calibration): from the stored measurement of
+    the same launch (`launch`: its label, say "bitcos_fast_kernel<5,32,bf16,
+    table>: 448 GEMVs in one launch"), or None if there is none or the kernel
+    sources changed since it was taken."""
+    kv = _stored(TRAFFIC_FILES.get(workload, []), launch)
+    try:
+        return None if kv is None else int(float(kv["traffic_bytes_per_launch"]))
+    except (KeyError, ValueError):
+        return None
 
 
 def launch_label(top, m):
@@ -690,6 +713,17 @@ def dominant_roofline(r, args, name):
     launch_gamma = 32 * CU_COUNT * CLOCK_HZ * per_launch_us * 1e-6 / top_weights
     hbm_term = 32 * alg_bytes / top_weights / (HBM_PEAK_GBS * 1e9 / (CU_COUNT * CLOCK_HZ))
     label = launch_label(top, m)
+    # VALU issue: every SIMD (4 per CU) issues one wave instruction per 4
+    # cycles (wave64 over 16 lanes; half-rate instructions count once, so
+    # this is a lower bound); the share of the launch's SIMD-cycles at the
+    # clock measured under load that the counted instructions occupy.
+    valu_n = stored_valu(name, label)
+    clk = (sclk or CLOCK_HZ / 1e6) * 1e6
+    valu = None if valu_n is None else {
+        "insts_per_launch": valu_n,
+        "busy_frac": round(4 * valu_n / (4 * CU_COUNT * clk * per_launch_us * 1e-6), 4),
+        "clock_mhz": round(clk / 1e6),
+    }
     return {
         # The roofline the metric is read against (weight bytes per second vs
         # HBM peak); what limits the kernel today is the larger two_term term,
@@ -707,6 +741,7 @@ def dominant_roofline(r, args, name):
         "weights_per_launch": int(top_weights),
         "two_term": {"cu_cycles_per_32w": round(launch_gamma, 4), "hbm_cu_cycles_per_32w": round(hbm_term, 4),
                      "larger_term": "instructions" if launch_gamma > hbm_term else "hbm"},
+        "valu": valu,
     }, sclk
 
 

@@ -177,6 +177,22 @@ def test_stored_traffic_only_for_the_measured_launch():
         assert bench.stored_traffic("qwen3_32b_layers", launch) == int(float(kv["traffic_bytes_per_launch"]))
 
 
+def test_stored_valu_count_follows_the_sources(monkeypatch):
+    """The stored SQ_INSTS_VALU count of the dominant launch is reported for
+    that launch only, and only while its kernel sources hash as measured."""
+    path = bench.COUNTER_FILES["qwen3_32b_layers"][0]
+    with open(path) as f:
+        kv = dict(line.split(":", 1) for line in f if ":" in line and not line.startswith("#"))
+    launch = kv["launch"].strip()
+    assert bench.stored_valu("qwen3_32b_layers", launch.replace(" GEMVs", "0 GEMVs")) is None
+    assert bench.stored_valu("no_such_set", launch) is None
+    measured = kv["kernel_source_hash"].strip()
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda kernel="bitcos_fast_kernel": measured)
+    assert bench.stored_valu("qwen3_32b_layers", launch) == int(float(kv["sq_insts_valu_per_launch"]))
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda kernel="bitcos_fast_kernel": "0" * 16)
+    assert bench.stored_valu("qwen3_32b_layers", launch) is None
+
+
 def test_kernel_source_hash_ignores_comments_only(tmp_path, monkeypatch):
     """A stored measurement stays valid across comment edits, not code edits."""
     import shutil
