@@ -4,7 +4,10 @@
 // and 2 bits per weight (Table I's 2-bit column).  Both use the BITCOS
 // kernel's work split (a wave step covers 64 / SEG rows; each lane owns
 // consecutive units of a row with its activations in VGPRs) so the three
-// kernels differ only in how they turn bytes into weights.
+// kernels differ only in how they turn bytes into weights.  Five-trit also
+// has 20-lane segments (three rows per step, the last four lanes idle) for
+// rows of 20 or 40 blocks, which power-of-two segments would leave up to
+// 3/8 idle at the few blocks per lane its activation registers allow.
 //
 //   five-trit  per byte, one LDS lookup gives its five weights as int8 (or
 //              bf16); four lookup tables hold the same five values shifted by
