@@ -330,17 +330,37 @@ def supported(entries, kind, m=1):
     return True
 
 
+class AddPartials:
+    """The step's last launch: the partial outputs of the split matrices'
+    later column blocks added into their outputs (bitcos_add_partials), one
+    call per stacked output buffer."""
+
+    def __init__(self, sums):
+        self.sums = sums  # [(Y [count, m, n], P [blocks - 1, count, m, n])]
+        self.entries, self.outputs = [], []
+        self.phase, self.tile, self.kernel = 1, ("partials",), "add_partials"
+
+    def run(self, stream=None):
+        from paper_2609_16338_amd import api
+        for y, parts in self.sums:
+            api.add_partials(y, parts, stream)
+
+
 def make_batches(entries, acts, kind):
     """One persistent launch per tile: the step's GEMVs grouped by kernel tile.
 
-    Column blocks of a long row (column_blocks) go to phases: every matrix's
-    first block (and every unsplit matrix) in phase 0, which writes the
-    outputs; block c in phase c, whose launches add onto them (_ADD output
-    mode) after the launches of phase c - 1 on the same stream, so each
-    output is a deterministic sum.  With m activation rows, BITCOS takes all
-    m in one launch (small-batch kernel); the five-trit and 2-bit layouts,
-    which have no small-batch kernel, take m batch-1 launches per tile, one
-    per activation row, as their m > 1 entry points do."""
+    Column blocks of a long row (column_blocks) all run in those launches:
+    a matrix's first block writes its output, block c + 1 writes slice c of
+    a partial buffer, and a last step (AddPartials) adds the slices into the
+    outputs in block order -- the same fp32 additions as the accumulating
+    output mode with one launch per block, so each output is a deterministic
+    sum.  The outputs of split matrices of one shape are stacked in one
+    buffer (and their partials in another) so that one call sums them all.
+    With m activation rows, BITCOS takes all m in one launch (small-batch
+    kernel); the five-trit and 2-bit layouts, which have no small-batch
+    kernel, take m batch-1 launches per tile, one per activation row, as
+    their m > 1 entry points do.  A batch's `outputs` are the matrices' final
+    outputs (what a check reads after the whole step)."""
     import torch
 
     from paper_2609_16338_amd import _native as N
@@ -352,11 +372,28 @@ def make_batches(entries, acts, kind):
     groups = {}
     for e in entries:
         info = api.describe(e[3], rows_per_launch, xd)
-        groups.setdefault((e[5][0], info.kernel, info.per_lane, info.seg_lanes), []).append(e)
-    ys = {}
+        groups.setdefault((info.kernel, info.per_lane, info.seg_lanes), []).append(e)
+    # Outputs: one [m, n] per matrix; split matrices of one (n, blocks) in a
+    # stacked [count, m, n] buffer with their partials in [blocks - 1, count, m, n].
+    nblocks, nrows = {}, {}
     for e in entries:
-        if (e[0], e[1]) not in ys:
-            ys[(e[0], e[1])] = torch.empty((m, e[2].n), dtype=torch.float32, device="cuda")
+        nblocks[(e[0], e[1])] = max(nblocks.get((e[0], e[1]), 0), e[5][0] + 1)
+        nrows[(e[0], e[1])] = e[2].n
+    ys, part, stacks = {}, {}, {}
+    for key, nb in nblocks.items():
+        if nb == 1:
+            ys[key] = torch.empty((m, nrows[key]), dtype=torch.float32, device="cuda")
+        else:
+            stacks.setdefault((nrows[key], nb), []).append(key)
+    sums = []
+    for (n, nb), keys in stacks.items():
+        y_all = torch.empty((len(keys), m, n), dtype=torch.float32, device="cuda")
+        p_all = torch.empty((nb - 1, len(keys), m, n), dtype=torch.float32, device="cuda")
+        for i, key in enumerate(keys):
+            ys[key] = y_all[i]
+            for c in range(1, nb):
+                part[key + (c,)] = p_all[c - 1, i]
+        sums.append((y_all, p_all))
     # Activations of a block: a contiguous copy of its columns (made once).
     blk = {}
 
@@ -372,26 +409,27 @@ def make_batches(entries, acts, kind):
         return blk[key]
 
     batches = []
-    order = sorted(groups.items(), key=lambda kv: (kv[0][0], -sum(e[3].n * e[3].k for e in kv[1])))
+    order = sorted(groups.items(), key=lambda kv: -sum(e[3].n * e[3].k for e in kv[1]))
     for key, ents in order:
-        phase = key[0]
         outs = [ys[(e[0], e[1])] for e in ents]
+        dsts = [outs[i] if e[5][0] == 0 else part[(e[0], e[1], e[5][0])] for i, e in enumerate(ents)]
         for r0 in range(0, m, rows_per_launch):
             r1 = r0 + rows_per_launch
             xs = [x_of(e)[0][r0:r1] for e in ents]  # [rows, k]: the batch takes rows from its shape
             xs = [x.reshape(-1) if rows_per_launch == 1 else x for x in xs]
             xss = [x_of(e)[1] for e in ents]
             xss = [None if v is None else v[r0:r1].reshape(-1) for v in xss]
-            b = api.Batch([e[3] for e in ents], [e[4] for e in ents], xs, [y[r0:r1].reshape(-1) for y in outs],
-                          xss if any(v is not None for v in xss) else None,
-                          y_mode=N.Y_F32 if phase == 0 else N.Y_F32_ADD)
-            b.tile = key[2:]
-            b.kernel = key[1]
-            b.phase = phase
+            b = api.Batch([e[3] for e in ents], [e[4] for e in ents], xs, [y[r0:r1].reshape(-1) for y in dsts],
+                          xss if any(v is not None for v in xss) else None, y_mode=N.Y_F32)
+            b.tile = key[1:]
+            b.kernel = key[0]
+            b.phase = 0
             b.entries = ents
             b.outputs = outs
             b.keep_x = blk
             batches.append(b)
+    if sums:
+        batches.append(AddPartials(sums))
     return batches
 
 

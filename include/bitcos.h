@@ -250,6 +250,22 @@ int bitcos_gemv_batch(const void* table_host, const void* table_dev, void* strea
 int bitcos_quantize_act(const void* x_bf16_dev, int32_t m, int32_t k, int8_t* q_dev,
                         float* scale_dev, void* stream);
 
+/* ---- partial outputs of split rows --------------------------------------
+ * bitcos_add_partials: y[i] += parts[0 * n + i] + parts[1 * n + i] + ... +
+ * parts[(nparts - 1) * n + i] for i < n, one fp32 addition per part, left to
+ * right.  For rows too long for one batch-1 tile, computed as column blocks
+ * (the row sum over K of Sec. II-C taken block by block): the first block's
+ * GEMV writes y (BITCOS_Y_F32), block c + 1's writes slice c of a device
+ * buffer [nparts][n] (also BITCOS_Y_F32), so every block can run in one
+ * launch, and this call adds the slices in block order -- the same fp32
+ * additions in the same order as the accumulating mode (BITCOS_Y_F32_ADD)
+ * with one launch per block.  y_dev and parts_dev are device fp32 buffers of
+ * n and nparts * n elements that do not overlap; several GEMVs' outputs can
+ * be summed in one call when their y and slices are laid out alike.
+ * Asynchronous on `stream`; allocates nothing.  Errors: E_ARG (null pointer,
+ * nparts < 1, n < 1), E_HIP. */
+int bitcos_add_partials(float* y_dev, const float* parts_dev, int32_t nparts, int64_t n, void* stream);
+
 /* ---- device-side BITCOS packer ------------------------------------------
  * The same blob bytes as bitcos_plan + bitcos_pack (Sec. II-A: presence
  * bitmap and compacted sign vector in row-major order, the unit offsets and

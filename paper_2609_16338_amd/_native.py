@@ -95,6 +95,7 @@ SIGNATURES = {
     "bit2_gemv": (ctypes.c_int, [_LP, _P, _I32, _P, _I32, _P, _P, _I32, _P]),
     "bitcos_describe": (ctypes.c_int, [_LP, _I32, _I32, ctypes.POINTER(LaunchInfo)]),
     "bitcos_quantize_act": (ctypes.c_int, [_P, _I32, _I32, _P, _P, _P]),
+    "bitcos_add_partials": (ctypes.c_int, [_P, _P, _I32, ctypes.c_int64, _P]),
     "bitcos_batch_bytes": (ctypes.c_size_t, [_I32]),
     "bitcos_batch_build": (ctypes.c_int, [_I32, _I32, _P, _P, _P, _P, _P, _I32, _I32, _P, _SZ]),
     "bitcos_gemv_batch": (ctypes.c_int, [_P, _P, _P]),

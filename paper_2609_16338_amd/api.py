@@ -249,6 +249,23 @@ def describe(L: Layout, m: int = 1, x_dtype: int = X_I8) -> LaunchInfo:
     return info
 
 
+def add_partials(y, parts, stream=None):
+    """Enqueue y += parts[0] + parts[1] + ... (fp32, in that order) on
+    `stream`: the partial outputs of a split row's later column blocks.
+    y: contiguous float32 cuda tensor of n elements; parts: contiguous float32
+    cuda tensor [nparts, ...] of nparts * n elements."""
+    import torch
+    for t, nm in ((y, "y"), (parts, "parts")):
+        if not t.is_cuda or not t.is_contiguous() or t.dtype != torch.float32:
+            raise ValueError(f"{nm} must be a contiguous float32 cuda tensor")
+    n = y.numel()
+    if parts.dim() < 1 or parts.shape[0] < 1 or parts.numel() != parts.shape[0] * n:
+        raise ValueError("parts must hold nparts slices of y's size")
+    N.check(N.lib().bitcos_add_partials(ctypes.c_void_p(y.data_ptr()), ctypes.c_void_p(parts.data_ptr()),
+                                        int(parts.shape[0]), n, _stream_handle(stream)), "bitcos_add_partials")
+    return y
+
+
 def quantize_activations(x, q, scale, stream=None):
     """Device int8 quantisation of bf16 activations per group of 128 (see bitcos.h)."""
     import torch

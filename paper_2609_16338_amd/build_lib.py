@@ -25,7 +25,7 @@ HIP_SOURCES = [
     "gemv_bitcos.hip", "gemv_bitcos_s4.hip", "gemv_bitcos_s8.hip", "gemv_bitcos_s16.hip",
     "gemv_bitcos_s32.hip", "gemv_bitcos_s64.hip", "gemv_fixed.hip", "fixed_trit5.hip", "fixed_bit2.hip",
     "gemv_bitcos_d4.hip", "gemv_bitcos_d8.hip", "gemv_bitcos_d16.hip", "gemv_bitcos_d32.hip", "gemv_bitcos_d64.hip",
-    "gemv_bitcos_mfma.hip", "batch.hip", "quantize.hip", "pack_device.hip",
+    "gemv_bitcos_mfma.hip", "batch.hip", "quantize.hip", "pack_device.hip", "partials.hip",
 ]
 HOST_SOURCES = ["host.cpp"]
 

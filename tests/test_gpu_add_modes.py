@@ -130,6 +130,46 @@ def test_column_blocks_add_up_to_the_whole_row(kind, fmt):
     assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))
     err = np.abs(outs[0].astype(np.float64) - ref)
     assert np.all(err <= bar + 1e-30), float((err / (bar + 1e-30)).max())
+    # The same blocks with blocks 1..4 written to a partial buffer and added by
+    # bitcos_add_partials: the same fp32 additions in the same order, so the
+    # same bits as the accumulating mode.
+    y = torch.full((1, n), float("nan"), dtype=torch.float32, device="cuda")
+    parts = torch.full((len(blocks) - 1, 1, n), float("nan"), dtype=torch.float32, device="cuda")
+    for c, (L, bd, xb, xsb) in enumerate(blocks):
+        api.gemv(L, bd, xb, y if c == 0 else parts[c - 1], xsb, N.Y_F32)
+    api.add_partials(y, parts)
+    torch.cuda.synchronize()
+    assert np.array_equal(y.cpu().numpy().view(np.uint32), outs[0].view(np.uint32))
+
+
+@pytest.mark.parametrize("n,nparts,offset", [(1, 1, 0), (7, 3, 0), (4096, 4, 0), (4096, 2, 1), (1000003, 4, 0),
+                                             (3 * 5120 * 64, 4, 0)])
+def test_add_partials_is_the_sum_in_block_order(n, nparts, offset):
+    """bitcos_add_partials: y[i] + parts[0][i] + ... + parts[P-1][i], one fp32
+    addition per part, left to right -- against the same additions in numpy,
+    bit-exact; four elements per thread on aligned buffers of a multiple of 4
+    elements, one otherwise (offset 1 misaligns both buffers)."""
+    rng = np.random.default_rng(n + nparts)
+    y0 = rng.standard_normal(n + offset).astype(np.float32)
+    p0 = rng.standard_normal((nparts, n + offset)).astype(np.float32)
+    ref = y0[offset:].copy()
+    for j in range(nparts):
+        ref = (ref + p0[j, offset:]).astype(np.float32)
+    yb = torch.from_numpy(y0).cuda()
+    pb = torch.from_numpy(p0.reshape(-1)).cuda()
+    y = yb[offset:]
+    if offset:
+        # parts as one buffer of nparts * n elements starting one element in
+        parts = torch.from_numpy(np.ascontiguousarray(p0[:, offset:]).reshape(-1))
+        pb = torch.empty(nparts * n + 1, dtype=torch.float32, device="cuda")
+        pb[1:].copy_(parts.cuda())
+        pview = pb[1:].view(nparts, n)
+    else:
+        pview = pb.view(nparts, n + offset)
+    say("add_partials", n, nparts, offset)
+    api.add_partials(y, pview)
+    torch.cuda.synchronize()
+    assert np.array_equal(y.cpu().numpy().view(np.uint32), ref.view(np.uint32))
 
 
 def test_add_modes_in_batch_tables():

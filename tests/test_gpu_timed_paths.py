@@ -31,6 +31,7 @@ pytestmark = [pytest.mark.gpu, pytest.mark.timeout(900)]
 torch = pytest.importorskip("torch")
 import bench  # noqa: E402
 from paper_2609_16338_amd import _native as N  # noqa: E402
+from paper_2609_16338_amd import api  # noqa: E402
 
 FMTS = (N.FMT_BITCOS, N.FMT_TRIT5, N.FMT_BIT2)
 
@@ -50,6 +51,11 @@ def max_resident_waves():
 def launch_units(b):
     """Work units of a batch's launch, from its host table header."""
     return int(b.host[32:40].view(np.int64)[0])
+
+
+def gemv_launches(batches):
+    """The step's GEMV launches (the last step may sum split rows' partials)."""
+    return [b for b in batches if isinstance(b, api.Batch)]
 
 
 HEADER_FIELDS = {"unit_is_step": 40, "m": 44, "any_xscale": 48, "any_grouped": 52, "row_offsets": 56,
@@ -81,7 +87,7 @@ def check_batches(batches, samples, host, kind, expect_multi_step=True):
     """Run the step twice (identical bits), then compare sampled rows of every
     GEMV with the oracle.  Returns the number of GEMVs checked."""
     bound_units = 2 * max_resident_waves()
-    for b in batches:
+    for b in gemv_launches(batches):
         if expect_multi_step:
             assert launch_units(b) > bound_units, (launch_units(b), bound_units, b.tile)
     outs = []
@@ -140,14 +146,14 @@ def test_bitnet_step_as_timed(bitnet_set, fmt, kind):
     streaming kernel's batch path, and the five-trit and 2-bit tables."""
     wk, packed, samples, acts, host = bitnet_set
     batches = bench.make_batches(packed[fmt], acts, kind)
-    say("bitnet", FMT_NAME(packed[fmt][0][3]), kind, [(b.tile, b.count, launch_units(b)) for b in batches])
+    say("bitnet", FMT_NAME(packed[fmt][0][3]), kind, [(b.tile, b.count, launch_units(b)) for b in gemv_launches(batches)])
     if fmt == N.FMT_BITCOS:
         # describe() names the kernel of a call without activation scales: the
         # matrix-core kernel for these per-tensor layouts.  The int8 variant
         # carries activation scales (header flag), which the launcher sends
         # to the streaming kernel instead.
-        assert all(b.kernel == N.KERNEL_MATRIX for b in batches)
-        assert all(header_flag(b, "any_xscale") == (kind == "int8") for b in batches)
+        assert all(b.kernel == N.KERNEL_MATRIX for b in gemv_launches(batches))
+        assert all(header_flag(b, "any_xscale") == (kind == "int8") for b in gemv_launches(batches))
     assert check_batches(batches, samples, host, kind) == len(packed[fmt])
 
 
@@ -155,8 +161,8 @@ def test_bitnet_step_as_timed(bitnet_set, fmt, kind):
 def qwen32_set():
     wk = wl.WORKLOADS["qwen3_32b_layers"]
     # Every launch of the batch-1 and M = 16 steps exceeds twice the resident
-    # waves: the smallest are the phases that add the down projections' later
-    # column blocks (five-trit: 3-row steps, layers x 1707 units).
+    # waves: a step runs its GEMVs, the down projections' column blocks
+    # included, as one launch per tile.
     layers = 26
     samples = {}
     say("building the Qwen3-32B-like set:", layers, "layers, 3 formats")
@@ -176,7 +182,7 @@ def test_qwen32_step_as_timed(qwen32_set, fmt, kind):
         assert fmt != N.FMT_BITCOS and kind == "bf16"
         pytest.skip("no kernel for bf16 rows of 25600 in this format (reported as null by the bench)")
     batches = bench.make_batches(packed[fmt], acts, kind)
-    say("qwen32", FMT_NAME(packed[fmt][0][3]), kind, [(b.tile, b.count, launch_units(b)) for b in batches])
+    say("qwen32", FMT_NAME(packed[fmt][0][3]), kind, [(b.tile, b.count, launch_units(b)) for b in gemv_launches(batches)])
     assert check_batches(batches, samples, host, kind) == len(packed[fmt])
 
 
@@ -188,8 +194,8 @@ def test_qwen32_small_batch_as_timed(qwen32_set, m, kind):
     wk, packed, samples = qwen32_set
     acts, host = oracle_acts(wk, m)
     batches = bench.make_batches(packed[N.FMT_BITCOS], acts, kind)
-    say("qwen32 small batch", m, kind, [(b.tile, b.count, launch_units(b)) for b in batches])
-    assert all(b.kernel == N.KERNEL_SMALL_BATCH for b in batches)
+    say("qwen32 small batch", m, kind, [(b.tile, b.count, launch_units(b)) for b in gemv_launches(batches)])
+    assert all(b.kernel == N.KERNEL_SMALL_BATCH for b in gemv_launches(batches))
     assert check_batches(batches, samples, host, kind) == len(packed[N.FMT_BITCOS])
 
 
@@ -198,7 +204,6 @@ def test_qwen32_small_batch_as_timed(qwen32_set, m, kind):
 def test_sweep_launch_as_timed(fmt, kind):
     """The zero-density sweep's launch: 40 device copies of one 8192 x 8192
     g128 matrix (z = 0.42) in one table; every copy's output is checked."""
-    from paper_2609_16338_amd import api
     cid, k, copies = 4, 8192, 40
     zi = wl.SWEEP_Z.index(0.42)
     spec = wl.sweep_spec(0.42)

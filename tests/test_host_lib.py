@@ -30,7 +30,7 @@ def header_functions():
 
 def test_library_loads_and_exports_every_declared_function():
     names = header_functions()
-    assert "bitcos_gemv" in names and "bit2_unpack" in names and len(names) == 23
+    assert "bitcos_gemv" in names and "bit2_unpack" in names and len(names) == 24
     lib = N.lib()
     for nm in names:
         assert hasattr(lib, nm), nm
@@ -198,6 +198,17 @@ def test_gemv_validation_happens_before_any_device_work():
     assert N.lib().bit2_gemv(ctypes.byref(Lt), dummy, 1, dummy, N.X_I8, None, dummy, N.Y_F32, None) == N.E_ARG
     assert N.lib().trit5_gemv(ctypes.byref(Lt), dummy, 17, dummy, N.X_I8, None, dummy, N.Y_F32, None) == N.E_ARG
     assert N.lib().trit5_gemv(ctypes.byref(Lt), dummy, 5, dummy, 9, None, dummy, N.Y_F32, None) == N.E_ARG
+
+
+def test_add_partials_argument_checks():
+    """bitcos_add_partials rejects null buffers, no parts and empty outputs
+    before anything is enqueued (no GPU needed)."""
+    f = N.lib().bitcos_add_partials
+    dummy = ctypes.c_void_p(16)
+    assert f(None, dummy, 1, 4, None) == N.E_ARG
+    assert f(dummy, None, 1, 4, None) == N.E_ARG
+    assert f(dummy, dummy, 0, 4, None) == N.E_ARG
+    assert f(dummy, dummy, 1, 0, None) == N.E_ARG
 
 
 def test_describe_small_batch():
