@@ -37,8 +37,9 @@ scaled by a plain copy's counters, stored under profiles/) while the kernel
 sources are unchanged; two_term: the launch's time and its bytes at peak HBM
 bandwidth in CU-cycles per 32 weights at the nominal 2.4 GHz, and which
 term is larger; valu: the launch's stored VALU instruction count (rocprofv3
-SQ_INSTS_VALU, same source rule) as a share of the SIMDs' issue cycles.  cpu_baseline: the oracle's decode + dense GEMV on whole
-layer-0 matrices on the host (about 12 s of work).
+SQ_INSTS_VALU, same source rule) as a share of the SIMDs' issue cycles.
+cpu_baseline: the oracle's decode + dense GEMV on whole layer-0 matrices on
+the host (about 12 s of work).
 
 Other modes print their own JSON line: --sweep (zero-density sweep on one
 8192 x 8192 matrix), --gamma (two-term roofline on cache-resident data),
@@ -188,7 +189,7 @@ def stored_traffic(workload, launch):
     """HBM bytes per launch of the dominant launch from the FETCH_SIZE / WRITE_SIZE
     passes (scaled by the copy calibration): from the stored measurement of
     the same launch (`launch`: its label, say "bitcos_fast_kernel<5,32,bf16,
-    table>: 448 GEMVs in one launch"), or None if there is none or the kernel
+    table>: 704 GEMVs in one launch"), or None if there is none or the kernel
     sources changed since it was taken."""
     kv = _stored(TRAFFIC_FILES.get(workload, []), launch)
     try:
